@@ -1,0 +1,206 @@
+"""Multi-Segment Attention (MSA) for AMD Instinct MI355X (gfx950).
+
+Thin ctypes binding of ``libmsa.so`` (C ABI in ``include/msa.h``).  It only
+marshals arguments: planning runs in the library's C++ planner and every
+step of the attention runs in the library's HIP kernels.  There is no CPU
+fallback: importing this package without a built library raises.
+
+Functions carry the C names: ``msa_plan``, ``msa_plan_info``,
+``msa_forward``, ``msa_plan_destroy``, ``msa_last_error``,
+``msa_plan_export``.  Device buffers are passed as objects with a
+``data_ptr()`` method (e.g. torch tensors) or as integer addresses; streams
+as ``hipStream_t`` integers or objects with ``cuda_stream`` (torch streams).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmsa.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_02964_amd.build`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+MSA_OK = 0
+MSA_ERR_INVALID_ARG = 1
+MSA_ERR_UNSUPPORTED = 2
+MSA_ERR_OUT_OF_MEMORY = 3
+MSA_ERR_DEVICE = 4
+MSA_PLAN_HOST_ONLY = 1
+MSA_PLAN_NO_AUTO_SPLIT = 2
+
+_i32, _i64, _f32, _f64, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
+
+
+class msa_shape(ctypes.Structure):
+    _fields_ = [("num_seqs", _i32), ("num_q_heads", _i32), ("num_kv_heads", _i32),
+                ("head_dim", _i32), ("block_size", _i32), ("max_blocks_per_seq", _i32),
+                ("num_blocks", _i32), ("scale", _f32),
+                ("q_stride_tok", _i64), ("q_stride_head", _i64),
+                ("o_stride_tok", _i64), ("o_stride_head", _i64),
+                ("k_stride_block", _i64), ("k_stride_head", _i64), ("k_stride_tok", _i64),
+                ("v_stride_block", _i64), ("v_stride_head", _i64), ("v_stride_dim", _i64)]
+
+
+class msa_plan_opts(ctypes.Structure):
+    _fields_ = [("q_tile_tokens", _i32), ("kv_split_tokens", _i32), ("flags", _i32),
+                ("reserved", _i32 * 5)]
+
+
+class msa_plan_info_t(ctypes.Structure):
+    _fields_ = [("total_q", _i64), ("num_work", _i64), ("num_tiles", _i64), ("num_merge", _i64),
+                ("max_splits", _i64), ("workspace_bytes", _i64), ("useful_flops", _f64),
+                ("tile_flops", _f64), ("planned_bytes", _f64), ("min_bytes", _f64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_lib.msa_plan.restype = _i32
+_lib.msa_plan.argtypes = [ctypes.POINTER(msa_shape), _P, _P, _P, _P,
+                          ctypes.POINTER(msa_plan_opts), _P, ctypes.POINTER(_P)]
+_lib.msa_plan_info.restype = _i32
+_lib.msa_plan_info.argtypes = [_P, ctypes.POINTER(msa_plan_info_t)]
+_lib.msa_forward.restype = _i32
+_lib.msa_forward.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.msa_plan_destroy.restype = None
+_lib.msa_plan_destroy.argtypes = [_P]
+_lib.msa_last_error.restype = ctypes.c_char_p
+_lib.msa_last_error.argtypes = []
+_lib.msa_plan_export.restype = _i32
+_lib.msa_plan_export.argtypes = [_P, _P, _P, _P]
+
+EXPORTED = ("msa_plan", "msa_plan_info", "msa_forward", "msa_plan_destroy", "msa_last_error",
+            "msa_plan_export")
+
+
+class MsaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[status {status}] {message}")
+        self.status = status
+
+
+def _check(status: int):
+    if status != MSA_OK:
+        raise MsaError(status, msa_last_error())
+
+
+def _addr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        try:
+            import torch
+            return int(torch.cuda.current_stream().cuda_stream)
+        except Exception:
+            return None
+    if isinstance(s, int):
+        return s
+    return int(s.cuda_stream)
+
+
+def _host_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+
+
+def msa_last_error() -> str:
+    return _lib.msa_last_error().decode()
+
+
+class Plan:
+    """Owning wrapper of an ``msa_plan_t`` handle."""
+
+    def __init__(self, handle: int, shape: msa_shape):
+        self.handle = handle
+        self.shape = shape
+
+    def info(self) -> dict:
+        return msa_plan_info(self)
+
+    def close(self):
+        if self.handle:
+            _lib.msa_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def msa_plan(shape: msa_shape, seq_kv_len: Sequence[int], seg_indptr: Sequence[int],
+             seg_start: Sequence[int], seg_len: Sequence[int], q_tile_tokens: int = 0,
+             kv_split_tokens: int = 0, flags: int = 0, stream=None) -> Plan:
+    """Validate the descriptors and build a plan (host arrays in, plan out)."""
+    kv = _host_i32(seq_kv_len)
+    ip = _host_i32(seg_indptr)
+    ss = _host_i32(seg_start)
+    sl = _host_i32(seg_len)
+    opts = msa_plan_opts(q_tile_tokens, kv_split_tokens, flags)
+    handle = _P()
+    st = _lib.msa_plan(ctypes.byref(shape), kv.ctypes.data, ip.ctypes.data,
+                       ss.ctypes.data if ss.size else None, sl.ctypes.data if sl.size else None,
+                       ctypes.byref(opts), None if flags & MSA_PLAN_HOST_ONLY else _stream(stream),
+                       ctypes.byref(handle))
+    _check(st)
+    return Plan(handle.value, shape)
+
+
+def msa_plan_info(plan: Plan) -> dict:
+    info = msa_plan_info_t()
+    _check(_lib.msa_plan_info(plan.handle, ctypes.byref(info)))
+    return info.as_dict()
+
+
+def msa_plan_export(plan: Plan):
+    """(row_pos [total_q], work [num_work, 8], merge [num_merge, 8]) as int32 arrays."""
+    info = msa_plan_info(plan)
+    row_pos = np.zeros(info["total_q"], np.int32)
+    work = np.zeros((info["num_work"], 8), np.int32)
+    merge = np.zeros((info["num_merge"], 8), np.int32)
+    _check(_lib.msa_plan_export(plan.handle, row_pos.ctypes.data if row_pos.size else None,
+                                work.ctypes.data if work.size else None,
+                                merge.ctypes.data if merge.size else None))
+    return row_pos, work, merge
+
+
+def msa_forward(plan: Plan, q, k_cache, v_cache, block_table, o, lse=None, workspace=None,
+                workspace_bytes: int = 0, stream=None) -> None:
+    """Enqueue MSA for one layer on ``stream`` (torch's current stream if None)."""
+    if workspace is not None and not workspace_bytes:
+        workspace_bytes = int(workspace.numel() * workspace.element_size())
+    _check(_lib.msa_forward(plan.handle, _addr(q), _addr(k_cache), _addr(v_cache),
+                            _addr(block_table), _addr(o), _addr(lse), _addr(workspace),
+                            int(workspace_bytes), _stream(stream)))
+
+
+def msa_plan_destroy(plan: Plan) -> None:
+    plan.close()
+
+
+def make_shape(num_seqs: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+               max_blocks_per_seq: int, num_blocks: int, scale: float,
+               q_strides=None, o_strides=None, k_strides=None, v_strides=None,
+               block_size: int = 16) -> msa_shape:
+    """msa_shape with contiguous defaults: q/o [total_q, Hq, d], K [blocks, Hkv, bs, d],
+    V [blocks, Hkv, d, bs].  Strides are (tok, head), (block, head, tok), (block, head, dim)."""
+    d, bs = head_dim, block_size
+    qs = q_strides or (num_q_heads * d, d)
+    os_ = o_strides or (num_q_heads * d, d)
+    ks = k_strides or (num_kv_heads * bs * d, bs * d, d)
+    vs = v_strides or (num_kv_heads * d * bs, d * bs, bs)
+    return msa_shape(num_seqs, num_q_heads, num_kv_heads, head_dim, block_size,
+                     max_blocks_per_seq, num_blocks, scale, qs[0], qs[1], os_[0], os_[1],
+                     ks[0], ks[1], ks[2], vs[0], vs[1], vs[2])

@@ -1,0 +1,210 @@
+// api.cpp -- the C ABI declared in include/msa.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/msa.h"
+#include "msa_internal.h"
+#include "plan.h"
+
+struct msa_plan_s {
+  msa::HostPlan hp;
+  bool host_only = true;
+  int device = -1;
+  std::vector<char> staging;  // host image of the device buffer (kept alive for the async copy)
+  char* dev = nullptr;        // device buffer: row_pos | work | merge
+  const int32_t* d_row_pos = nullptr;
+  const msa::WorkItem* d_work = nullptr;
+  const msa::MergeItem* d_merge = nullptr;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+msa_status set_error(msa_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* msa_last_error(void) { return g_last_error.c_str(); }
+
+msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int32_t* seg_indptr,
+                    const int32_t* seg_start, const int32_t* seg_len, const msa_plan_opts* opts,
+                    void* hip_stream, msa_plan_t* out) {
+  if (!out) return set_error(MSA_ERR_INVALID_ARG, "msa_plan: out must be non-null");
+  *out = nullptr;
+  msa_plan_s* plan = new (std::nothrow) msa_plan_s();
+  if (!plan) return set_error(MSA_ERR_OUT_OF_MEMORY, "msa_plan: host allocation failed");
+  std::string err;
+  msa_status st;
+  try {
+    st = msa::build_plan(shape, seq_kv_len, seg_indptr, seg_start, seg_len, opts, &plan->hp, &err);
+  } catch (const std::bad_alloc&) {
+    st = MSA_ERR_OUT_OF_MEMORY;
+    err = "host allocation failed while planning";
+  }
+  if (st != MSA_OK) {
+    delete plan;
+    return set_error(st, "msa_plan: " + err);
+  }
+  plan->host_only = opts && (opts->flags & MSA_PLAN_HOST_ONLY);
+  if (!plan->host_only) {
+    const msa::HostPlan& hp = plan->hp;
+    const size_t n_row = hp.row_pos.size() * sizeof(int32_t);
+    const size_t n_work = hp.work.size() * sizeof(msa::WorkItem);
+    const size_t n_merge = hp.merge.size() * sizeof(msa::MergeItem);
+    const size_t off_work = align_up(n_row, 256);
+    const size_t off_merge = off_work + align_up(n_work, 256);
+    const size_t bytes = std::max<size_t>(off_merge + n_merge, 256);
+    try {
+      plan->staging.assign(bytes, 0);
+    } catch (const std::bad_alloc&) {
+      delete plan;
+      return set_error(MSA_ERR_OUT_OF_MEMORY, "msa_plan: host allocation failed");
+    }
+    if (n_row) std::memcpy(plan->staging.data(), hp.row_pos.data(), n_row);
+    if (n_work) std::memcpy(plan->staging.data() + off_work, hp.work.data(), n_work);
+    if (n_merge) std::memcpy(plan->staging.data() + off_merge, hp.merge.data(), n_merge);
+    if (hipGetDevice(&plan->device) != hipSuccess) {
+      delete plan;
+      return set_error(MSA_ERR_DEVICE, "msa_plan: hipGetDevice failed");
+    }
+    void* dev = nullptr;
+    if (hipMalloc(&dev, bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      delete plan;
+      return set_error(MSA_ERR_OUT_OF_MEMORY, "msa_plan: hipMalloc of the plan buffer failed");
+    }
+    plan->dev = static_cast<char*>(dev);
+    if (hipMemcpyAsync(dev, plan->staging.data(), bytes, hipMemcpyHostToDevice,
+                       static_cast<hipStream_t>(hip_stream)) != hipSuccess) {
+      (void)hipGetLastError();
+      (void)hipFree(dev);
+      delete plan;
+      return set_error(MSA_ERR_DEVICE, "msa_plan: upload of the plan buffer failed");
+    }
+    plan->d_row_pos = reinterpret_cast<const int32_t*>(plan->dev);
+    plan->d_work = reinterpret_cast<const msa::WorkItem*>(plan->dev + off_work);
+    plan->d_merge = reinterpret_cast<const msa::MergeItem*>(plan->dev + off_merge);
+  }
+  *out = plan;
+  return MSA_OK;
+}
+
+msa_status msa_plan_info(msa_plan_t plan, msa_plan_info_t* info) {
+  if (!plan || !info) return set_error(MSA_ERR_INVALID_ARG, "msa_plan_info: null argument");
+  const msa::HostPlan& hp = plan->hp;
+  info->total_q = hp.total_q;
+  info->num_work = (int64_t)hp.work.size();
+  info->num_tiles = hp.num_tiles;
+  info->num_merge = (int64_t)hp.merge.size();
+  info->max_splits = hp.max_splits;
+  info->workspace_bytes = hp.workspace_bytes;
+  info->useful_flops = hp.useful_flops;
+  info->tile_flops = hp.tile_flops;
+  info->planned_bytes = hp.planned_bytes;
+  info->min_bytes = hp.min_bytes;
+  return MSA_OK;
+}
+
+msa_status msa_plan_export(msa_plan_t plan, int32_t* row_pos, int32_t* work, int32_t* merge) {
+  if (!plan) return set_error(MSA_ERR_INVALID_ARG, "msa_plan_export: null plan");
+  const msa::HostPlan& hp = plan->hp;
+  if (row_pos && !hp.row_pos.empty())
+    std::memcpy(row_pos, hp.row_pos.data(), hp.row_pos.size() * sizeof(int32_t));
+  if (work && !hp.work.empty())
+    std::memcpy(work, hp.work.data(), hp.work.size() * sizeof(msa::WorkItem));
+  if (merge && !hp.merge.empty())
+    std::memcpy(merge, hp.merge.data(), hp.merge.size() * sizeof(msa::MergeItem));
+  return MSA_OK;
+}
+
+void msa_plan_destroy(msa_plan_t plan) {
+  if (!plan) return;
+  if (plan->dev) (void)hipFree(plan->dev);
+  delete plan;
+}
+
+msa_status msa_forward(msa_plan_t plan, const void* q, const void* k_cache, const void* v_cache,
+                       const int32_t* block_table, void* o, float* lse, void* workspace,
+                       size_t workspace_bytes, void* hip_stream) {
+  if (!plan) return set_error(MSA_ERR_INVALID_ARG, "msa_forward: null plan");
+  if (plan->host_only)
+    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: plan was built with MSA_PLAN_HOST_ONLY");
+  const msa::HostPlan& hp = plan->hp;
+  if (hp.work.empty()) return MSA_OK;  // no query rows: nothing to do
+  if (!q || !k_cache || !v_cache || !block_table || !o)
+    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: q, k_cache, v_cache, block_table, o must be non-null");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(o, 16) ||
+      !aligned(block_table, 4) || (lse && !aligned(lse, 4)))
+    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: q/k/v/o must be 16-byte aligned");
+  if ((size_t)hp.workspace_bytes > workspace_bytes)
+    return set_error(MSA_ERR_INVALID_ARG,
+                     "msa_forward: workspace too small (need " + std::to_string(hp.workspace_bytes) +
+                         " bytes)");
+  if (hp.workspace_bytes > 0 && (!workspace || !aligned(workspace, 16)))
+    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: workspace must be non-null and 16-byte aligned");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
+    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: current device differs from the plan's device");
+
+  const msa_shape& s = hp.shape;
+  msa::AttnParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_cache);
+  p.v = static_cast<const uint16_t*>(v_cache);
+  p.block_table = block_table;
+  p.row_pos = plan->d_row_pos;
+  p.work = plan->d_work;
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.ws = static_cast<float*>(workspace);
+  p.q_st = s.q_stride_tok;
+  p.q_sh = s.q_stride_head;
+  p.o_st = s.o_stride_tok;
+  p.o_sh = s.o_stride_head;
+  p.k_sb = s.k_stride_block;
+  p.k_sh = s.k_stride_head;
+  p.k_st = s.k_stride_tok;
+  p.v_sb = s.v_stride_block;
+  p.v_sh = s.v_stride_head;
+  p.v_sd = s.v_stride_dim;
+  p.max_blocks = s.max_blocks_per_seq;
+  p.num_q_heads = s.num_q_heads;
+  p.group = hp.group;
+  p.tile_tokens = hp.tile_tokens;
+  p.scale_log2 = s.scale * 1.4426950408889634f;
+  int rc = msa::launch_attn(p, s.head_dim, (int)hp.work.size(), hip_stream);
+  if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string("msa_forward: attention launch failed: ") +
+                                                    hipGetErrorString((hipError_t)rc));
+  if (!hp.merge.empty()) {
+    msa::MergeParams m{};
+    m.merge = plan->d_merge;
+    m.ws = static_cast<const float*>(workspace);
+    m.o = static_cast<uint16_t*>(o);
+    m.lse = lse;
+    m.o_st = s.o_stride_tok;
+    m.o_sh = s.o_stride_head;
+    m.num_q_heads = s.num_q_heads;
+    m.group = hp.group;
+    rc = msa::launch_merge(m, s.head_dim, (int)hp.merge.size(), hip_stream);
+    if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string("msa_forward: merge launch failed: ") +
+                                                      hipGetErrorString((hipError_t)rc));
+  }
+  return MSA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,324 @@
+// attn.hip -- gfx950 kernels of Multi-Segment Attention.
+//
+// msa_attn: one workgroup (4 waves, 256 threads) per work item = up to 128
+// query rows of one sequence sharing one KV head, over one key range.  Per
+// 64-key step:
+//   - paged gather: the 4 cache blocks of the step are looked up in the block
+//     table and copied to LDS with 16-byte loads (K as [key][d], V as [d][key]
+//     since the V cache is channel-major inside a block), double buffered;
+//   - S^T = K Q^T on v_mfma_f32_32x32x16_bf16.  K is the A operand, so in the
+//     result each lane holds one query row (column) and 16 of the 32 keys:
+//     row max and row sum need one exchange with the lane 32 apart only;
+//   - per-row causal limit: key j is visible to the row at absolute position
+//     p iff j <= p (applied only on steps that reach past the smallest
+//     position of the wave);
+//   - online softmax in fp32 (exp2 domain, scale * log2(e) folded in);
+//   - O^T += V^T P^T on the same MFMA: P is the B operand and is packed to
+//     bf16 straight from the score registers.  The A-operand row order of K is
+//     permuted (bits 2 and 3 of the row index swapped) so that the 8 scores a
+//     lane feeds to one PV step are 8 consecutive keys, matching a single
+//     16-byte LDS read of V^T.
+// msa_merge: combines the per-split partials of a split tile by log-sum-exp.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdint>
+
+#include "msa_internal.h"
+
+namespace msa {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <int D>
+struct Tile {
+  static constexpr int kPitchK = D * 2 + 16;        // bytes per key row of the K tile
+  static constexpr int kPitchV = kKvStep * 2 + 16;  // bytes per channel row of the V^T tile
+  static constexpr int kBytesK = kKvStep * kPitchK;
+  static constexpr int kBytesV = D * kPitchV;
+  static constexpr int kStage = kBytesK + kBytesV;
+  static constexpr int kRounds = kKvStep * D / 8 / 256;  // 16-byte chunks per thread, per tensor
+};
+
+__device__ __forceinline__ int swap_bits23(int m) {
+  return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+// max / sum of x over the lane pair (l, l ^ 32)
+__device__ __forceinline__ float pair_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
+  using T = Tile<D>;
+  __shared__ __attribute__((aligned(16))) char smem[2 * T::kStage];
+
+  const WorkItem w = p.work[blockIdx.x];
+  if (w.nrows == 0) return;  // padding item (uniform over the workgroup)
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, hl = lane >> 5, ln = lane & 31;
+  const int G = p.group;
+  const int r = wave * 32 + ln;  // tile row
+  const int t = r / G, hh = r - t * G;
+  const bool valid = t < w.nrows;
+  const int tok = w.row0 + t;
+  const int head = w.kv_head * G + hh;
+  const int pos = valid ? p.row_pos[tok] : -1;
+
+  // wave-wide smallest and largest causal limit (wave-uniform branches)
+  int pmin = valid ? pos : INT_MAX, pmax = pos;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    pmin = min(pmin, __shfl_xor(pmin, off));
+    pmax = max(pmax, __shfl_xor(pmax, off));
+  }
+
+  // Q fragments (B operand): row r, channels kk*16 + hl*8 .. +8
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t* qrow = p.q + (int64_t)tok * p.q_st + (int64_t)head * p.q_sh + hl * 8;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      if (valid) {
+        qf[kk] = *reinterpret_cast<const bf16x8*>(qrow + kk * 16);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) qf[kk][j] = (__bf16)0.0f;
+      }
+    }
+  }
+
+  const int32_t* bt = p.block_table + (int64_t)w.seq * p.max_blocks;
+  const uint16_t* kbase = p.k + (int64_t)w.kv_head * p.k_sh;
+  const uint16_t* vbase = p.v + (int64_t)w.kv_head * p.v_sh;
+
+  uint4 kr[T::kRounds], vr[T::kRounds];
+  // global -> registers for the step starting at key kb; blocks at or past
+  // kv_hi are not read (their block-table entries need not be valid)
+  auto load = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < T::kRounds; ++i) {
+      const int c = tid + 256 * i;
+      const int key = c / (D / 8), dch = c % (D / 8), page = key >> 4;
+      if (kb + page * kBlockSize < w.kv_hi) {
+        const int64_t blk = bt[(kb >> 4) + page];
+        kr[i] = *reinterpret_cast<const uint4*>(kbase + blk * p.k_sb + (key & 15) * p.k_st + dch * 8);
+      } else {
+        kr[i] = make_uint4(0, 0, 0, 0);
+      }
+      const int vpage = c / (2 * D), rem = c % (2 * D), ch = rem >> 1, half = rem & 1;
+      if (kb + vpage * kBlockSize < w.kv_hi) {
+        const int64_t blk = bt[(kb >> 4) + vpage];
+        vr[i] = *reinterpret_cast<const uint4*>(vbase + blk * p.v_sb + ch * p.v_sd + half * 8);
+      } else {
+        vr[i] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto store = [&](char* st) {
+#pragma unroll
+    for (int i = 0; i < T::kRounds; ++i) {
+      const int c = tid + 256 * i;
+      const int key = c / (D / 8), dch = c % (D / 8);
+      *reinterpret_cast<uint4*>(st + key * T::kPitchK + dch * 16) = kr[i];
+      const int vpage = c / (2 * D), rem = c % (2 * D), ch = rem >> 1, half = rem & 1;
+      *reinterpret_cast<uint4*>(st + T::kBytesK + ch * T::kPitchV + (vpage * 16 + half * 8) * 2) = vr[i];
+    }
+  };
+
+  float m_run = -__builtin_inff(), l_run = 0.0f;
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.0f;
+
+  const int nsteps = (w.kv_hi - w.kv_lo + kKvStep - 1) / kKvStep;
+  load(w.kv_lo);
+  store(smem);
+  __syncthreads();
+
+  for (int it = 0; it < nsteps; ++it) {
+    const int kb = w.kv_lo + it * kKvStep;
+    const char* cur = smem + (it & 1) * T::kStage;
+    char* nxt = smem + ((it + 1) & 1) * T::kStage;
+    const bool more = it + 1 < nsteps;
+    if (more) load(kb + kKvStep);
+
+    if (kb <= pmax) {  // some row of this wave sees a key of this step
+      // S^T = K Q^T: two 32-key tiles
+      f32x16 s[2];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[kt][i] = 0.0f;
+        const char* krow = cur + (kt * 32 + swap_bits23(ln)) * T::kPitchK + hl * 16;
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + kk * 32);
+          s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[kt], 0, 0, 0);
+        }
+      }
+      // lane (hl, ln), register i of tile kt holds key kb + kt*32 + (i/8)*16 + hl*8 + i%8
+      const bool need_mask = kb + kKvStep - 1 > pmin;
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float x = s[kt][i] * p.scale_log2;
+          if (need_mask) {
+            const int key = kb + kt * 32 + (i >> 3) * 16 + hl * 8 + (i & 7);
+            x = key <= pos ? x : -__builtin_inff();
+          }
+          s[kt][i] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = pair_max(mx);
+      const float m_new = fmaxf(m_run, mx);
+      const float m_use = m_new == -__builtin_inff() ? 0.0f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      // P is rounded to bf16 for the PV product; the row sum adds the same
+      // rounded values, so the normalised weights sum to one exactly and the
+      // output stays a convex combination of the values
+      float ls = 0.0f;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const __bf16 e = (__bf16)__builtin_amdgcn_exp2f(s[kt][i] - m_use);
+          ls += (float)e;
+          pb[kt * 2 + (i >> 3)][i & 7] = e;
+        }
+      l_run = l_run * alpha + ls;
+      m_run = m_new;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+      // O^T += V^T P^T: 4 steps of 16 keys
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) {
+        const char* vrow = cur + T::kBytesK + (dt * 32 + ln) * T::kPitchV + hl * 16;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(vrow + ks * 32);
+          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[dt], 0, 0, 0);
+        }
+      }
+    }
+
+    if (more) store(nxt);
+    __syncthreads();
+  }
+
+  // epilogue: lane (hl, ln) holds row r, channels dt*32 + (i/4)*8 + hl*4 + i%4
+  const float l_tot = pair_sum(l_run);
+  if (!valid) return;
+  if (w.out_slot < 0) {
+    const float inv = 1.0f / l_tot;
+    uint16_t* orow = p.o + (int64_t)tok * p.o_st + (int64_t)head * p.o_sh;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = (__bf16)(oacc[dt][g4 * 4 + j] * inv);
+        *reinterpret_cast<bf16x4*>(orow + dt * 32 + g4 * 8 + hl * 4) = v;
+      }
+    if (p.lse && hl == 0)
+      p.lse[(int64_t)tok * p.num_q_heads + head] = (m_run + __log2f(l_tot)) * kLn2;
+  } else {
+    float* slot = p.ws + (int64_t)w.out_slot * kTileRows * (D + 1);
+    const bool empty = !(l_tot > 0.0f);  // no visible key in this split
+    const float inv = empty ? 0.0f : 1.0f / l_tot;
+    float* orow = slot + r * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        f32x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = oacc[dt][g4 * 4 + j] * inv;
+        *reinterpret_cast<f32x4*>(orow + dt * 32 + g4 * 8 + hl * 4) = v;
+      }
+    if (hl == 0)
+      slot[kTileRows * D + r] = empty ? -__builtin_inff() : (m_run + __log2f(l_tot)) * kLn2;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void msa_merge_kernel(MergeParams p) {
+  constexpr int kThreadsPerRow = D / 4;
+  constexpr int kRowsPerPass = 256 / kThreadsPerRow;
+  const MergeItem mi = p.merge[blockIdx.x];
+  const int G = p.group;
+  const int rows = mi.nrows * G;
+  const int sub = threadIdx.x % kThreadsPerRow;
+  const int64_t slot_f = (int64_t)kTileRows * (D + 1);
+  for (int r = threadIdx.x / kThreadsPerRow; r < rows; r += kRowsPerPass) {
+    const int t = r / G, hh = r - t * G;
+    const int tok = mi.row0 + t, head = mi.kv_head * G + hh;
+    float mx = -__builtin_inff();
+    for (int s = 0; s < mi.nsplit; ++s)
+      mx = fmaxf(mx, p.ws[(int64_t)(mi.slot0 + s) * slot_f + kTileRows * D + r]);
+    const float mu = mx == -__builtin_inff() ? 0.0f : mx;
+    float L = 0.0f;
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int s = 0; s < mi.nsplit; ++s) {
+      const float* base = p.ws + (int64_t)(mi.slot0 + s) * slot_f;
+      const float wgt = __builtin_amdgcn_exp2f((base[kTileRows * D + r] - mu) * kLog2e);
+      L += wgt;
+      const f32x4 os = *reinterpret_cast<const f32x4*>(base + r * D + sub * 4);
+      acc += wgt * os;
+    }
+    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+    bf16x4 v;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = (__bf16)(acc[j] * inv);
+    *reinterpret_cast<bf16x4*>(p.o + (int64_t)tok * p.o_st + (int64_t)head * p.o_sh + sub * 4) = v;
+    if (p.lse && sub == 0) p.lse[(int64_t)tok * p.num_q_heads + head] = mu + __logf(L);
+  }
+}
+
+}  // namespace
+
+int launch_attn(const AttnParams& p, int head_dim, int num_work, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (num_work <= 0) return 0;
+  if (head_dim == 128)
+    hipLaunchKernelGGL(msa_attn_kernel<128>, dim3(num_work), dim3(256), 0, s, p);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(msa_attn_kernel<64>, dim3(num_work), dim3(256), 0, s, p);
+  else
+    return (int)hipErrorInvalidValue;
+  return (int)hipGetLastError();
+}
+
+int launch_merge(const MergeParams& p, int head_dim, int num_merge, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (num_merge <= 0) return 0;
+  if (head_dim == 128)
+    hipLaunchKernelGGL(msa_merge_kernel<128>, dim3(num_merge), dim3(256), 0, s, p);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(msa_merge_kernel<64>, dim3(num_merge), dim3(256), 0, s, p);
+  else
+    return (int)hipErrorInvalidValue;
+  return (int)hipGetLastError();
+}
+
+}  // namespace msa

@@ -1,0 +1,297 @@
+// plan.cpp -- host planner: segment descriptors -> per-row positions and the
+// workgroup work list of one fused MSA launch.
+//
+// The paper dispatches every request segment to a group of CTAs inside a
+// single kernel and gives each token its own "equivalent seq_len" through a
+// precomputed array (Sec. 4.1).  Here:
+//   1. rows: each packed query row gets its absolute position (its causal
+//      limit is position + 1 keys);
+//   2. tiles: consecutive rows of one sequence are packed into tiles of up to
+//      128 / G tokens (G = Hq / Hkv query heads share one KV head), across
+//      segment gaps as long as the keys masked for the earlier rows stay a
+//      small fraction of the tile's work;
+//   3. units: tile x KV head, keys [0, max position in tile + 1);
+//   4. key splits: units much longer than the average share of a workgroup
+//      slot are cut into 64-aligned key ranges, merged later by log-sum-exp;
+//   5. order: (sequence, KV head) groups are spread over the 8 XCDs (blockIdx
+//      i runs on XCD i % 8) so tiles sharing K/V share one XCD's L2, longest
+//      first inside each XCD.
+#include "plan.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+
+namespace msa {
+namespace {
+
+constexpr int kXcds = 8;
+constexpr int kSlots = 256 * 2;          // CUs x resident workgroups per CU
+constexpr double kWasteFrac = 0.125;     // masked keys allowed per tile, relative
+constexpr int64_t kMinSplitKeys = 1024;  // never split below this many keys
+
+msa_status fail(std::string* err, msa_status st, const std::string& msg) {
+  *err = msg;
+  return st;
+}
+
+bool aligned8(int64_t x) { return x > 0 && (x % 8) == 0; }
+
+struct Unit {
+  int32_t seq, kv_head, row0, nrows, kv_hi;
+};
+
+}  // namespace
+
+msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int32_t* seg_indptr,
+                      const int32_t* seg_start, const int32_t* seg_len, const msa_plan_opts* opts,
+                      HostPlan* out, std::string* err) {
+  if (!shape || !out) return fail(err, MSA_ERR_INVALID_ARG, "shape and out must be non-null");
+  const msa_shape& s = *shape;
+  msa_plan_opts o{};
+  if (opts) o = *opts;
+  for (int i = 0; i < 5; ++i)
+    if (o.reserved[i] != 0) return fail(err, MSA_ERR_INVALID_ARG, "opts.reserved must be zero");
+  if (o.flags & ~(MSA_PLAN_HOST_ONLY | MSA_PLAN_NO_AUTO_SPLIT))
+    return fail(err, MSA_ERR_INVALID_ARG, "unknown opts.flags bits");
+
+  if (s.num_seqs < 0) return fail(err, MSA_ERR_INVALID_ARG, "num_seqs < 0");
+  if (s.num_q_heads < 1 || s.num_kv_heads < 1)
+    return fail(err, MSA_ERR_INVALID_ARG, "head counts must be >= 1");
+  if (s.num_q_heads % s.num_kv_heads != 0)
+    return fail(err, MSA_ERR_INVALID_ARG, "num_q_heads must be a multiple of num_kv_heads");
+  const int32_t G = s.num_q_heads / s.num_kv_heads;
+  if (G > kTileRows) return fail(err, MSA_ERR_UNSUPPORTED, "num_q_heads / num_kv_heads > 128");
+  if (s.head_dim <= 0) return fail(err, MSA_ERR_INVALID_ARG, "head_dim <= 0");
+  if (s.head_dim != 64 && s.head_dim != 128)
+    return fail(err, MSA_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (s.block_size <= 0) return fail(err, MSA_ERR_INVALID_ARG, "block_size <= 0");
+  if (s.block_size != kBlockSize) return fail(err, MSA_ERR_UNSUPPORTED, "block_size must be 16");
+  if (s.max_blocks_per_seq < 0 || s.num_blocks < 0)
+    return fail(err, MSA_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be >= 0");
+  if (!std::isfinite(s.scale)) return fail(err, MSA_ERR_INVALID_ARG, "scale must be finite");
+  if (!aligned8(s.q_stride_tok) || !aligned8(s.q_stride_head) || !aligned8(s.o_stride_tok) ||
+      !aligned8(s.o_stride_head) || !aligned8(s.k_stride_block) || !aligned8(s.k_stride_head) ||
+      !aligned8(s.k_stride_tok) || !aligned8(s.v_stride_block) || !aligned8(s.v_stride_head) ||
+      !aligned8(s.v_stride_dim))
+    return fail(err, MSA_ERR_INVALID_ARG, "strides must be positive multiples of 8 elements");
+  int32_t tile_tokens = kTileRows / G;
+  if (o.q_tile_tokens < 0 || o.q_tile_tokens > tile_tokens)
+    return fail(err, MSA_ERR_INVALID_ARG, "q_tile_tokens must be in [0, 128 / (Hq/Hkv)]");
+  if (o.q_tile_tokens > 0) tile_tokens = o.q_tile_tokens;
+  if (o.kv_split_tokens < 0 || o.kv_split_tokens % kKvStep != 0)
+    return fail(err, MSA_ERR_INVALID_ARG, "kv_split_tokens must be a non-negative multiple of 64");
+
+  const int32_t B = s.num_seqs;
+  if (B > 0 && (!seq_kv_len || !seg_indptr))
+    return fail(err, MSA_ERR_INVALID_ARG, "seq_kv_len and seg_indptr must be non-null");
+  if (B > 0 && seg_indptr[0] != 0) return fail(err, MSA_ERR_INVALID_ARG, "seg_indptr[0] != 0");
+  for (int32_t b = 0; b < B; ++b)
+    if (seg_indptr[b + 1] < seg_indptr[b])
+      return fail(err, MSA_ERR_INVALID_ARG, "seg_indptr must be non-decreasing");
+  const int64_t nseg = B > 0 ? seg_indptr[B] : 0;
+  if (nseg > 0 && (!seg_start || !seg_len))
+    return fail(err, MSA_ERR_INVALID_ARG, "seg_start and seg_len must be non-null");
+
+  // 1. rows and their absolute positions
+  HostPlan& P = *out;
+  P = HostPlan{};
+  P.shape = s;
+  P.group = G;
+  P.tile_tokens = tile_tokens;
+  std::vector<int64_t> seq_row0(B + 1, 0);
+  std::vector<int32_t> seq_maxpos(B, -1);
+  int64_t total = 0;
+  const int64_t cap = (int64_t)s.max_blocks_per_seq * s.block_size;
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t L = seq_kv_len[b];
+    if (L < 0 || L > cap)
+      return fail(err, MSA_ERR_INVALID_ARG,
+                  "seq_kv_len[" + std::to_string(b) + "] outside [0, max_blocks_per_seq*16]");
+    int64_t prev_end = 0;
+    seq_row0[b] = total;
+    for (int32_t k = seg_indptr[b]; k < seg_indptr[b + 1]; ++k) {
+      const int64_t st = seg_start[k], n = seg_len[k];
+      if (n < 1) return fail(err, MSA_ERR_INVALID_ARG, "segment " + std::to_string(k) + " is empty");
+      if (st < prev_end)
+        return fail(err, MSA_ERR_INVALID_ARG,
+                    "segment " + std::to_string(k) + " overlaps or is out of order");
+      if (st + n > L)
+        return fail(err, MSA_ERR_INVALID_ARG,
+                    "segment " + std::to_string(k) + " extends past seq_kv_len");
+      total += n;
+      if (total >= ((int64_t)1 << 31)) return fail(err, MSA_ERR_INVALID_ARG, "total_q >= 2^31");
+      prev_end = st + n;
+      seq_maxpos[b] = (int32_t)(st + n - 1);
+    }
+  }
+  seq_row0[B] = total;
+  P.total_q = total;
+  P.row_pos.resize((size_t)total);
+  {
+    int64_t r = 0;
+    for (int32_t b = 0; b < B; ++b)
+      for (int32_t k = seg_indptr[b]; k < seg_indptr[b + 1]; ++k)
+        for (int32_t t = 0; t < seg_len[k]; ++t) P.row_pos[(size_t)r++] = seg_start[k] + t;
+  }
+
+  // 2-3. tiles and units
+  std::vector<Unit> units;
+  const int32_t Hkv = s.num_kv_heads, d = s.head_dim;
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t lo = seq_row0[b], hi = seq_row0[b + 1];
+    int64_t i = lo;
+    while (i < hi) {
+      const int64_t first = i;
+      double useful = (double)P.row_pos[(size_t)i] + 1.0, waste = 0.0;
+      int32_t cnt = 1;
+      ++i;
+      while (i < hi && cnt < tile_tokens) {
+        const double step = (double)P.row_pos[(size_t)i] - (double)P.row_pos[(size_t)(i - 1)];
+        const double nw = waste + cnt * step;
+        const double nu = useful + (double)P.row_pos[(size_t)i] + 1.0;
+        if (nw > kWasteFrac * nu && nw > (double)kKvStep * tile_tokens) break;
+        waste = nw;
+        useful = nu;
+        ++cnt;
+        ++i;
+      }
+      const int32_t kv_hi = P.row_pos[(size_t)(first + cnt - 1)] + 1;
+      for (int32_t g = 0; g < Hkv; ++g) units.push_back(Unit{b, g, (int32_t)first, cnt, kv_hi});
+    }
+  }
+  P.num_tiles = (int64_t)units.size();
+
+  // 4. key splits
+  auto steps = [](int64_t keys) { return (keys + kKvStep - 1) / kKvStep; };
+  int64_t split_keys = 0;  // 0: no split
+  if (o.kv_split_tokens > 0) {
+    split_keys = o.kv_split_tokens;
+  } else if (!(o.flags & MSA_PLAN_NO_AUTO_SPLIT) && !units.empty()) {
+    double total_steps = 0;
+    for (const Unit& u : units) total_steps += (double)(steps(u.kv_hi) + 1);
+    // aim at >= 2 work items per workgroup slot for the longest units
+    const int64_t share = (int64_t)std::ceil(total_steps / (2.0 * kSlots)) * kKvStep;
+    split_keys = std::max<int64_t>(kMinSplitKeys, share);
+  }
+  struct Piece {
+    int32_t unit, lo, hi, slot;
+  };
+  std::vector<Piece> pieces;
+  int64_t slots = 0;
+  for (size_t ui = 0; ui < units.size(); ++ui) {
+    const Unit& u = units[ui];
+    int64_t nsplit = 1;
+    if (split_keys > 0) {
+      // auto mode splits only units clearly longer than the share
+      const bool forced = o.kv_split_tokens > 0;
+      if (forced ? (u.kv_hi > split_keys) : (u.kv_hi > 2 * split_keys))
+        nsplit = (u.kv_hi + split_keys - 1) / split_keys;
+    }
+    if (nsplit <= 1) {
+      pieces.push_back(Piece{(int32_t)ui, 0, u.kv_hi, -1});
+      continue;
+    }
+    // equal 64-aligned chunks, last one takes the remainder
+    int64_t chunk = ((u.kv_hi + nsplit - 1) / nsplit + kKvStep - 1) / kKvStep * kKvStep;
+    nsplit = (u.kv_hi + chunk - 1) / chunk;
+    const int32_t slot0 = (int32_t)slots;
+    for (int64_t k = 0; k < nsplit; ++k) {
+      const int64_t a = k * chunk, e = std::min<int64_t>(u.kv_hi, (k + 1) * chunk);
+      pieces.push_back(Piece{(int32_t)ui, (int32_t)a, (int32_t)e, (int32_t)(slots++)});
+    }
+    P.merge.push_back(MergeItem{u.seq, u.kv_head, u.row0, u.nrows, (int32_t)nsplit, slot0, 0, 0});
+    P.max_splits = std::max<int64_t>(P.max_splits, nsplit);
+  }
+  P.num_slots = slots;
+  P.workspace_bytes = slots * slot_floats(d) * (int64_t)sizeof(float);
+
+  // 5. order: groups (seq, kv head) -> XCD queues, longest first
+  const int64_t ngroups = (int64_t)B * Hkv;
+  std::vector<double> gcost((size_t)ngroups, 0.0);
+  auto pcost = [&](const Piece& p) { return (double)(steps(p.hi - p.lo) + 1); };
+  for (const Piece& p : pieces) {
+    const Unit& u = units[(size_t)p.unit];
+    gcost[(size_t)((int64_t)u.seq * Hkv + u.kv_head)] += pcost(p);
+  }
+  double total_cost = 0;
+  for (double c : gcost) total_cost += c;
+  std::vector<std::vector<int32_t>> queue(kXcds);
+  std::vector<double> load(kXcds, 0.0);
+  auto least_loaded = [&]() {
+    return (int)(std::min_element(load.begin(), load.end()) - load.begin());
+  };
+  std::vector<int32_t> order(pieces.size());
+  std::iota(order.begin(), order.end(), 0);
+  // A group keeps one XCD unless it alone is a large part of an XCD's work
+  // (few groups): then its pieces are spread by cost like independent work.
+  std::vector<int64_t> gorder((size_t)ngroups);
+  std::iota(gorder.begin(), gorder.end(), 0);
+  std::stable_sort(gorder.begin(), gorder.end(),
+                   [&](int64_t a, int64_t b) { return gcost[(size_t)a] > gcost[(size_t)b]; });
+  std::vector<int32_t> ghome((size_t)ngroups, -1);
+  const double big = 0.5 * total_cost / kXcds;
+  for (int64_t gi : gorder) {
+    if (gcost[(size_t)gi] <= 0 || gcost[(size_t)gi] > big) continue;
+    const int x = least_loaded();
+    ghome[(size_t)gi] = x;
+    load[(size_t)x] += gcost[(size_t)gi];
+  }
+  // pieces sorted: by group cost (desc), then own cost (desc), then index
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    const Unit& ua = units[(size_t)pieces[(size_t)a].unit];
+    const Unit& ub = units[(size_t)pieces[(size_t)b].unit];
+    const int64_t ga = (int64_t)ua.seq * Hkv + ua.kv_head, gb = (int64_t)ub.seq * Hkv + ub.kv_head;
+    if (ga != gb && gcost[(size_t)ga] != gcost[(size_t)gb])
+      return gcost[(size_t)ga] > gcost[(size_t)gb];
+    if (ga != gb) return ga < gb;
+    return pcost(pieces[(size_t)a]) > pcost(pieces[(size_t)b]);
+  });
+  for (int32_t pi : order) {
+    const Unit& u = units[(size_t)pieces[(size_t)pi].unit];
+    const int64_t gi = (int64_t)u.seq * Hkv + u.kv_head;
+    int x = ghome[(size_t)gi];
+    if (x < 0) {
+      x = least_loaded();
+      load[(size_t)x] += pcost(pieces[(size_t)pi]);
+    }
+    queue[(size_t)x].push_back(pi);
+  }
+  size_t rounds = 0;
+  for (const auto& q : queue) rounds = std::max(rounds, q.size());
+  // trim trailing XCDs with nothing in the last round so a small problem
+  // does not launch a whole row of padding
+  P.work.reserve(rounds * kXcds);
+  for (size_t k = 0; k < rounds; ++k)
+    for (int x = 0; x < kXcds; ++x) {
+      if (k < queue[(size_t)x].size()) {
+        const Piece& p = pieces[(size_t)queue[(size_t)x][k]];
+        const Unit& u = units[(size_t)p.unit];
+        P.work.push_back(WorkItem{u.seq, u.kv_head, u.row0, u.nrows, p.lo, p.hi, p.slot, 0});
+      } else {
+        P.work.push_back(WorkItem{0, 0, 0, 0, 0, 0, -1, 0});
+      }
+    }
+  while (!P.work.empty() && P.work.back().nrows == 0) P.work.pop_back();
+
+  // figures
+  const double hq = s.num_q_heads;
+  for (int64_t r = 0; r < total; ++r) P.useful_flops += 4.0 * d * hq * ((double)P.row_pos[(size_t)r] + 1);
+  const double qo_bytes = 2.0 * 2.0 * (double)total * hq * d;  // Q read + O write, bf16
+  P.planned_bytes = qo_bytes;
+  for (const WorkItem& w : P.work) {
+    if (w.nrows == 0) continue;
+    const double keys = (double)(w.kv_hi - w.kv_lo);
+    P.planned_bytes += keys * d * 2.0 * 2.0;
+    // waves whose 32 rows are all empty skip every step
+    const double rows = (double)((w.nrows * G + 31) / 32 * 32);
+    P.tile_flops += 4.0 * d * rows * (double)steps(w.kv_hi - w.kv_lo) * kKvStep;
+  }
+  P.min_bytes = qo_bytes;
+  for (int32_t b = 0; b < B; ++b)
+    if (seq_maxpos[b] >= 0) P.min_bytes += (double)(seq_maxpos[b] + 1) * d * 2.0 * 2.0 * Hkv;
+  return MSA_OK;
+}
+
+}  // namespace msa

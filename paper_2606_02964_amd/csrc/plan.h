@@ -1,0 +1,33 @@
+// plan.h -- host planner of the MSA library (no HIP calls).
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "../../include/msa.h"
+#include "msa_internal.h"
+
+namespace msa {
+
+struct HostPlan {
+  msa_shape shape{};
+  int32_t group = 1;        // G = Hq / Hkv
+  int32_t tile_tokens = 0;  // query tokens per tile
+  int64_t total_q = 0;
+  std::vector<int32_t> row_pos;   // [total_q]
+  std::vector<WorkItem> work;     // launch order (blockIdx.x)
+  std::vector<MergeItem> merge;
+  int64_t num_tiles = 0;          // tiles x kv heads before splitting
+  int64_t max_splits = 1;
+  int64_t num_slots = 0;          // workspace partial slots
+  int64_t workspace_bytes = 0;
+  double useful_flops = 0, tile_flops = 0, planned_bytes = 0, min_bytes = 0;
+};
+
+// Validates the inputs and fills *out.  On error returns the status and a
+// message in *err; *out is then unspecified.
+msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int32_t* seg_indptr,
+                      const int32_t* seg_start, const int32_t* seg_len, const msa_plan_opts* opts,
+                      HostPlan* out, std::string* err);
+
+}  // namespace msa

@@ -1,0 +1,357 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+* the library loads and exports every function ``include/msa.h`` declares;
+* the planner (run with MSA_PLAN_HOST_ONLY, so nothing touches a device):
+  per-row absolute positions are bit-exact, every (row, q head) is covered
+  by tiles whose key ranges partition [0, kv_hi) with kv_hi >= position + 1,
+  no item reads a block past the last visible one, splits and merge items
+  are consistent, plans are deterministic, malformed descriptors get the
+  documented status codes;
+* a CPU interpreter of the *plan* (per work item partial softmax, then the
+  log-sum-exp merge) reproduces the oracle, which pins the planner's key
+  ranges and the merge rule without a GPU.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "msa.h")
+
+
+@pytest.fixture(scope="module")
+def msa():
+    import paper_2606_02964_amd as m
+    return m
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(msa_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function(msa):
+    names = declared_functions()
+    assert {"msa_plan", "msa_forward", "msa_plan_info", "msa_plan_destroy",
+            "msa_last_error", "msa_plan_export"} <= set(names)
+    lib = ctypes.CDLL(msa.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in msa.h but not exported"
+    nm = subprocess.run(["nm", "-D", "--defined-only", msa.LIB_PATH], capture_output=True,
+                        text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (msa_\w+)", nm))
+    assert set(names) <= exported
+    assert set(msa.EXPORTED) == set(names)
+
+
+def shape_of(msa, inst):
+    return msa.make_shape(inst.num_seqs, inst.num_q_heads, inst.num_kv_heads, inst.head_dim,
+                          inst.max_blocks_per_seq, inst.num_blocks, inst.scale)
+
+
+def host_plan(msa, inst, **kw):
+    flags = kw.pop("flags", 0) | msa.MSA_PLAN_HOST_ONLY
+    return msa.msa_plan(shape_of(msa, inst), inst.seq_kv_len, inst.seg_indptr, inst.seg_start,
+                        inst.seg_len, flags=flags, **kw)
+
+
+def expected_positions(inst):
+    pos = []
+    for b in range(inst.num_seqs):
+        for (s, n) in inst.segments(b):
+            pos.extend(range(s, s + n))
+    return np.asarray(pos, dtype=np.int32)
+
+
+def row_sequence(inst):
+    seq = []
+    for b in range(inst.num_seqs):
+        seq.extend([b] * int(inst.seg_len[inst.seg_indptr[b]:inst.seg_indptr[b + 1]].sum()))
+    return np.asarray(seq, dtype=np.int64)
+
+
+def check_plan(inst, row_pos, work, merge, info, G):
+    """Structural invariants of a plan."""
+    total = inst.total_q
+    assert np.array_equal(row_pos, expected_positions(inst))
+    rseq = row_sequence(inst)
+    Hkv = inst.num_kv_heads
+    # coverage per (row, kv head): key pieces in order
+    pieces = {}
+    slots_seen = set()
+    for w in work:
+        seq, g, row0, nrows, lo, hi, slot, flags = (int(x) for x in w)
+        if nrows == 0:
+            continue
+        assert 0 <= g < Hkv and 0 <= row0 and row0 + nrows <= total
+        assert nrows * G <= 128
+        assert (rseq[row0:row0 + nrows] == seq).all(), "tile crosses a sequence"
+        assert lo % 64 == 0 and 0 <= lo < hi
+        tile_max = int(row_pos[row0:row0 + nrows].max())
+        assert hi <= tile_max + 1, "item reads keys past the tile's last visible key"
+        assert (hi + 15) // 16 <= (int(inst.seq_kv_len[seq]) + 15) // 16
+        if slot >= 0:
+            assert slot not in slots_seen
+            slots_seen.add(slot)
+        key = (row0, nrows, g)
+        pieces.setdefault(key, []).append((lo, hi, slot))
+    covered = np.zeros((total, Hkv), dtype=np.int32)
+    merged = {(int(m[2]), int(m[3]), int(m[1])): m for m in merge}
+    for (row0, nrows, g), ps in pieces.items():
+        ps.sort()
+        assert ps[0][0] == 0
+        for a, b in zip(ps, ps[1:]):
+            assert a[1] == b[0], "key ranges of a tile must be contiguous"
+        hi = ps[-1][1]
+        assert (row_pos[row0:row0 + nrows] + 1 <= hi).all()
+        if len(ps) == 1:
+            assert ps[0][2] == -1
+        else:
+            m = merged[(row0, nrows, g)]
+            assert int(m[4]) == len(ps)
+            assert [p[2] for p in ps] == list(range(int(m[5]), int(m[5]) + len(ps)))
+        covered[row0:row0 + nrows, g] += 1
+    assert (covered == 1).all(), "every (row, kv head) must be in exactly one tile"
+    assert len(merged) == len(merge)
+    assert info["total_q"] == total
+    assert info["workspace_bytes"] == len(slots_seen) * 128 * (inst.head_dim + 1) * 4
+    useful = 4.0 * inst.head_dim * inst.num_q_heads * float((row_pos.astype(np.float64) + 1).sum())
+    assert abs(info["useful_flops"] - useful) <= 1e-9 * max(1.0, useful)
+
+
+PLAN_CASES = [
+    dict(seed=1, num_seqs=3, num_q_heads=4, num_kv_heads=2, head_dim=64, max_len=700, max_segs=6),
+    dict(seed=2, num_seqs=5, num_q_heads=32, num_kv_heads=8, head_dim=128, max_len=3000, max_segs=9),
+    dict(seed=3, num_seqs=2, num_q_heads=6, num_kv_heads=2, head_dim=128, max_len=500, max_segs=4),
+    dict(seed=4, num_seqs=4, num_q_heads=8, num_kv_heads=8, head_dim=64, max_len=129, max_segs=3),
+]
+
+
+@pytest.mark.parametrize("case", PLAN_CASES)
+@pytest.mark.parametrize("split", [0, 64, 192, 1024])
+def test_plan_structure(msa, case, split):
+    inst = workloads.make_random(keep_logical=False, **case)
+    plan = host_plan(msa, inst, kv_split_tokens=split)
+    info = plan.info()
+    row_pos, work, merge = msa.msa_plan_export(plan)
+    check_plan(inst, row_pos, work, merge, info, inst.num_q_heads // inst.num_kv_heads)
+    if split:
+        assert info["num_merge"] > 0 or all(int(w[5]) <= split for w in work if w[3] > 0)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_plan_structure_named_workloads(msa, cfg):
+    inst = make_layout_only(cfg)
+    plan = host_plan(msa, inst)
+    info = plan.info()
+    row_pos, work, merge = msa.msa_plan_export(plan)
+    check_plan(inst, row_pos, work, merge, info, inst.num_q_heads // inst.num_kv_heads)
+    # a plan's masked waste stays small
+    assert info["tile_flops"] <= 1.6 * info["useful_flops"] + 4 * 128 * inst.head_dim * 64 * len(work)
+
+
+def make_layout_only(cfg):
+    """The named workload's descriptors without drawing its (large) tensors."""
+    name, layout = workloads.CONFIGS[cfg]
+    rng = np.random.Generator(np.random.PCG64(cfg))
+    lens, segs, heads = layout(rng)
+
+    class L:
+        pass
+    inst = L()
+    inst.num_seqs = len(lens)
+    inst.num_q_heads, inst.num_kv_heads, inst.head_dim = (heads["num_q_heads"],
+                                                          heads["num_kv_heads"], heads["head_dim"])
+    inst.block_size = 16
+    inst.scale = 1.0 / np.sqrt(inst.head_dim)
+    inst.seq_kv_len = np.asarray(lens, np.int32)
+    starts, ls, indptr = [], [], [0]
+    for sg in segs:
+        for (s, n) in sg:
+            starts.append(s)
+            ls.append(n)
+        indptr.append(len(starts))
+    inst.seg_start = np.asarray(starts, np.int32)
+    inst.seg_len = np.asarray(ls, np.int32)
+    inst.seg_indptr = np.asarray(indptr, np.int32)
+    inst.max_blocks_per_seq = max(-(-L // 16) for L in lens)
+    inst.num_blocks = sum(-(-L // 16) for L in lens)
+    inst.total_q = int(inst.seg_len.sum())
+    inst.segments = lambda b: [(int(inst.seg_start[k]), int(inst.seg_len[k]))
+                               for k in range(inst.seg_indptr[b], inst.seg_indptr[b + 1])]
+    return inst
+
+
+def test_named_workload_sizes():
+    """Row counts of the named workloads match their definitions."""
+    assert make_layout_only(1).total_q == 128
+    assert make_layout_only(2).total_q == 8 * (128 * 16 + 512)
+    assert make_layout_only(3).total_q == 16 * 64 * 32
+    assert make_layout_only(4).total_q == 2 * (2048 + 4096)
+
+
+def test_plan_is_deterministic(msa):
+    inst = workloads.make_random(keep_logical=False, **PLAN_CASES[1])
+    a = msa.msa_plan_export(host_plan(msa, inst))
+    b = msa.msa_plan_export(host_plan(msa, inst))
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_empty_and_zero_segment_sequences(msa):
+    inst = workloads.make_layout(5, [10, 40, 0], [[], [(3, 5)], []], 4, 2, 64)
+    plan = host_plan(msa, inst)
+    info = plan.info()
+    row_pos, work, merge = msa.msa_plan_export(plan)
+    assert info["total_q"] == 5 and list(row_pos) == [3, 4, 5, 6, 7]
+    check_plan(inst, row_pos, work, merge, info, 2)
+    none = workloads.make_layout(6, [16], [[]], 2, 2, 64)
+    p2 = host_plan(msa, none)
+    assert p2.info()["total_q"] == 0 and p2.info()["num_work"] == 0
+
+
+def test_forward_rejects_host_only_plan_and_null_plan(msa):
+    inst = workloads.make_config(1)
+    plan = host_plan(msa, inst)
+    with pytest.raises(msa.MsaError) as e:
+        msa.msa_forward(plan, 16, 16, 16, 16, 16, stream=0)
+    assert e.value.status == msa.MSA_ERR_INVALID_ARG
+    assert "HOST_ONLY" in msa.msa_last_error()
+    null = msa.Plan(None, None)
+    with pytest.raises(msa.MsaError):
+        msa.msa_forward(null, 16, 16, 16, 16, 16, stream=0)
+
+
+def _bad(inst, what):
+    kv = inst.seq_kv_len.copy()
+    ip = inst.seg_indptr.copy()
+    ss = inst.seg_start.copy()
+    sl = inst.seg_len.copy()
+    if what == "overlap":
+        ss[1] = ss[0] + sl[0] - 1
+    elif what == "unsorted":
+        ss[0], ss[1] = ss[1], ss[0]
+        sl[0], sl[1] = sl[1], sl[0]
+    elif what == "empty":
+        sl[1] = 0
+    elif what == "past_end":
+        ss[1] = kv[0] - sl[1] + 1
+    elif what == "negative_start":
+        ss[0] = -1
+    elif what == "kv_len_too_big":
+        kv[0] = inst.max_blocks_per_seq * 16 + 1
+    elif what == "indptr":
+        ip[0] = 1
+    return kv, ip, ss, sl
+
+
+@pytest.mark.parametrize("what", ["overlap", "unsorted", "empty", "past_end", "negative_start",
+                                  "kv_len_too_big", "indptr"])
+def test_plan_rejects_malformed_segments(msa, what):
+    inst = workloads.make_layout(7, [256], [[(10, 30), (100, 40)]], 4, 2, 64)
+    kv, ip, ss, sl = _bad(inst, what)
+    with pytest.raises(msa.MsaError) as e:
+        msa.msa_plan(shape_of(msa, inst), kv, ip, ss, sl, flags=msa.MSA_PLAN_HOST_ONLY)
+    assert e.value.status == msa.MSA_ERR_INVALID_ARG
+    assert msa.msa_last_error()
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, 2), ("head_dim", 0, 1), ("block_size", 32, 2), ("block_size", 0, 1),
+    ("num_kv_heads", 3, 1), ("num_q_heads", 0, 1), ("q_stride_tok", 12, 1),
+    ("v_stride_dim", 0, 1), ("scale", float("nan"), 1), ("num_seqs", -1, 1)])
+def test_plan_rejects_bad_shapes(msa, field, value, status):
+    inst = workloads.make_layout(8, [256], [[(10, 30)]], 4, 2, 64)
+    sh = shape_of(msa, inst)
+    setattr(sh, field, value)
+    with pytest.raises(msa.MsaError) as e:
+        msa.msa_plan(sh, inst.seq_kv_len, inst.seg_indptr, inst.seg_start, inst.seg_len,
+                     flags=msa.MSA_PLAN_HOST_ONLY)
+    assert e.value.status == status
+
+
+def test_plan_rejects_bad_options(msa):
+    inst = workloads.make_layout(9, [256], [[(10, 30)]], 4, 2, 64)
+    for kw in (dict(kv_split_tokens=100), dict(q_tile_tokens=65), dict(kv_split_tokens=-64)):
+        with pytest.raises(msa.MsaError) as e:
+            host_plan(msa, inst, **kw)
+        assert e.value.status == msa.MSA_ERR_INVALID_ARG
+    big_group = workloads.make_layout(10, [64], [[(0, 4)]], 256, 1, 64)
+    with pytest.raises(msa.MsaError) as e:
+        host_plan(msa, big_group)
+    assert e.value.status == msa.MSA_ERR_UNSUPPORTED
+
+
+# --------------------------------------------------------------------------
+# CPU interpreter of a plan (float64), compared with the oracle
+# --------------------------------------------------------------------------
+
+def interpret_plan(inst, row_pos, work, merge):
+    """Run the plan's work items with exact float64 math: each item gives a
+    partial (o, lse) over its key range per row; split tiles are combined by
+    log-sum-exp.  Reads K/V through the block table like the kernel does."""
+    from workloads import bf16_bits_to_f32
+    G = inst.num_q_heads // inst.num_kv_heads
+    d = inst.head_dim
+    q = bf16_bits_to_f32(inst.q).astype(np.float64)
+    out_o = np.full((inst.total_q, inst.num_q_heads, d), np.nan)
+    out_l = np.full((inst.total_q, inst.num_q_heads), np.nan)
+    partial = {}
+    for w in work:
+        seq, g, row0, nrows, lo, hi, slot, _ = (int(x) for x in w)
+        if nrows == 0:
+            continue
+        keys = np.arange(lo, hi)
+        blk = inst.block_table[seq, keys // 16]
+        K = bf16_bits_to_f32(inst.k_cache[blk, g, keys % 16, :]).astype(np.float64)
+        V = bf16_bits_to_f32(inst.v_cache[blk, g, :, keys % 16]).astype(np.float64)
+        for t in range(nrows):
+            row = row0 + t
+            vis = keys <= row_pos[row]
+            for hh in range(G):
+                h = g * G + hh
+                s = inst.scale * (K @ q[row, h])
+                s = np.where(vis, s, -np.inf)
+                m = s.max()
+                if m == -np.inf:
+                    o, l = np.zeros(d), -np.inf
+                else:
+                    e = np.exp(s - m)
+                    o, l = (e @ V) / e.sum(), m + np.log(e.sum())
+                if slot < 0:
+                    out_o[row, h], out_l[row, h] = o, l
+                else:
+                    partial[(slot, row, h)] = (o, l)
+    for m in merge:
+        seq, g, row0, nrows, nsplit, slot0 = (int(x) for x in m[:6])
+        for t in range(nrows):
+            row = row0 + t
+            for hh in range(G):
+                h = g * G + hh
+                parts = [partial[(slot0 + k, row, h)] for k in range(nsplit)]
+                ls = np.array([p[1] for p in parts])
+                mx = ls.max()
+                wts = np.exp(ls - mx)
+                out_o[row, h] = sum(wt * p[0] for wt, p in zip(wts, parts)) / wts.sum()
+                out_l[row, h] = mx + np.log(wts.sum())
+    return out_o, out_l
+
+
+@pytest.mark.parametrize("split", [0, 64, 128])
+@pytest.mark.parametrize("case", PLAN_CASES[:2] + PLAN_CASES[3:])
+def test_plan_interpreter_matches_oracle(msa, oracle_lib, case, split):
+    case = dict(case, max_len=min(case["max_len"], 400))
+    inst = workloads.make_random(keep_logical=False, **case)
+    plan = host_plan(msa, inst, kv_split_tokens=split)
+    row_pos, work, merge = msa.msa_plan_export(plan)
+    io, il = interpret_plan(inst, row_pos, work, merge)
+    o, l = oracle_lib.forward(inst)
+    np.testing.assert_allclose(io, o, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(il, l, rtol=0, atol=1e-12)

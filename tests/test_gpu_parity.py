@@ -1,0 +1,293 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle on MI355X.
+
+Bar (bf16 inputs, bf16 output): max-abs <= 1e-2 and mean-abs <= 1e-3 over
+every compared element; lse within 2^-9 + 1e-4 (natural log); index handling
+bit-exact (permuting physical blocks, poisoning blocks nobody references
+and garbage past the context end leave the output bit-identical).
+"""
+import copy
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from msa_pins import repermute
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on a CPU-only host with -m gpu
+    pytest.skip("no GPU visible", allow_module_level=True)
+
+from gpu_helpers import (LSE_ABS, MAX_ABS, MEAN_ABS, DeviceInstance, bf16_to_f32,  # noqa: E402
+                         dev_bf16, errors, run)
+import paper_2606_02964_amd as msa  # noqa: E402
+
+
+def check_full(inst, oracle_lib, **plan_kw):
+    o, lse, plan = run(DeviceInstance(inst), **plan_kw)
+    ro, rl = oracle_lib.forward(inst)
+    go = bf16_to_f32(o)
+    assert np.isfinite(go).all(), "some output rows were not written"
+    mx, mean = errors(go, ro)
+    lerr = float(np.abs(lse.cpu().numpy().astype(np.float64) - rl).max())
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
+    assert lerr <= LSE_ABS, lerr
+    return go, lse.cpu().numpy(), plan
+
+
+def test_config1_full_parity(oracle_lib):
+    inst = workloads.make_config(1)
+    check_full(inst, oracle_lib)
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13])
+def test_config1_other_seeds(oracle_lib, seed):
+    check_full(workloads.make_config(1, seed=seed), oracle_lib)
+
+
+RANDOM = [
+    # seed, B, Hq, Hkv, d, max_len, max_segs
+    (101, 3, 4, 4, 64, 700, 5),
+    (102, 4, 32, 8, 128, 1500, 8),
+    (103, 2, 64, 8, 128, 1200, 3),
+    (104, 5, 8, 1, 64, 333, 4),
+    (105, 3, 6, 2, 128, 900, 6),     # G = 3: tiles with unused rows
+    (106, 6, 2, 2, 128, 70, 3),      # short sequences, ragged last blocks
+    (107, 2, 16, 16, 64, 2100, 4),   # MHA, many tiles per sequence
+]
+
+
+@pytest.mark.parametrize("case", RANDOM)
+@pytest.mark.parametrize("split", [0, 64, 320])
+def test_random_full_parity(oracle_lib, case, split):
+    seed, B, Hq, Hkv, d, max_len, max_segs = case
+    inst = workloads.make_random(seed, num_seqs=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d,
+                                 max_len=max_len, max_segs=max_segs, keep_logical=False)
+    _, _, plan = check_full(inst, oracle_lib, kv_split_tokens=split)
+    max_keys = max((s + n for b in range(inst.num_seqs) for (s, n) in inst.segments(b)), default=0)
+    if split and max_keys > split:
+        assert plan.info()["num_merge"] > 0
+
+
+def test_block_aligned_and_adjacent_segments(oracle_lib):
+    inst = workloads.make_layout(31, [1024, 777], [[(0, 16), (16, 32), (64, 64), (512, 512)],
+                                                  [(0, 1), (1, 1), (400, 377)]], 32, 8, 128)
+    check_full(inst, oracle_lib)
+
+
+def test_prefill_and_decode_layouts(oracle_lib):
+    inst = workloads.make_layout(32, [1000, 513, 64], [[(0, 1000)], [(512, 1)], [(63, 1)]], 8, 2, 128)
+    check_full(inst, oracle_lib)
+
+
+def test_sequences_sharing_physical_prefix_blocks(oracle_lib):
+    """Two sequences whose block tables point at the same physical blocks for
+    a shared prefix (prefix caching, Sec. 2.2)."""
+    inst = workloads.make_layout(33, [300, 300], [[(100, 50), (250, 50)], [(128, 40), (290, 10)]],
+                                 8, 2, 64, permute_blocks=True)
+    inst.block_table = inst.block_table.copy()
+    inst.block_table[1, :8] = inst.block_table[0, :8]   # first 128 positions shared
+    check_full(inst, oracle_lib)
+
+
+def test_zero_rows_launches_nothing():
+    inst = workloads.make_layout(34, [64, 32], [[], []], 4, 2, 64)
+    d = DeviceInstance(inst)
+    plan = d.plan()
+    assert plan.info()["num_work"] == 0
+    o = torch.empty((0, 4, 64), dtype=torch.bfloat16, device="cuda")
+    msa.msa_forward(plan, d.q, d.k, d.v, d.bt, o, None, None)
+    torch.cuda.synchronize()
+
+
+def _sample_items(inst, n, seed):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    rows = rng.integers(0, inst.total_q, size=n)
+    # first and last rows of every sequence, every row at position 0
+    starts = np.cumsum(np.r_[0, [inst.seg_len[inst.seg_indptr[b]:inst.seg_indptr[b + 1]].sum()
+                                 for b in range(inst.num_seqs)]])
+    extra = [s for s in starts[:-1]] + [e - 1 for e in starts[1:] if e > 0]
+    rows = np.r_[rows, np.asarray(extra, dtype=np.int64)]
+    rows = rows[(rows >= 0) & (rows < inst.total_q)]
+    heads = rng.integers(0, inst.num_q_heads, size=rows.shape[0])
+    return rows.astype(np.int64), heads.astype(np.int32)
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
+def test_named_workload_sampled_parity(oracle_lib, cfg):
+    """Full-size workloads in the benchmark's launch configuration (automatic
+    plan): every output finite and inside the convex hull of V, sampled
+    (row, head) items against the oracle."""
+    inst = workloads.make_config(cfg)
+    d = DeviceInstance(inst)
+    o, lse, plan = run(d)
+    go = o.float()
+    assert torch.isfinite(go).all().item(), "some output rows were not written"
+    assert torch.isfinite(lse).all().item()
+    vmax = float(np.abs(workloads.bf16_bits_to_f32(inst.v_cache)).max())
+    assert float(go.abs().max()) <= vmax * (1 + 2 ** -7)
+    rows, heads = _sample_items(inst, 1500, seed=cfg)
+    ro, rl = oracle_lib.forward(inst, rows=rows, heads=heads)
+    gsel = go[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    mx, mean = errors(gsel, ro)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
+    lsel = lse[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    assert float(np.abs(lsel - rl).max()) <= LSE_ABS
+
+
+def test_config4_forced_split_matches_unsplit(oracle_lib):
+    inst = workloads.make_config(4)
+    d = DeviceInstance(inst)
+    o1, l1, p1 = run(d, flags=msa.MSA_PLAN_NO_AUTO_SPLIT)
+    o2, l2, p2 = run(d, kv_split_tokens=4096)
+    assert p1.info()["num_merge"] == 0 and p2.info()["num_merge"] > 0
+    diff = (o1.float() - o2.float()).abs()
+    # both are within one bf16 rounding of the same fp32 value
+    assert float(diff.max()) <= 2 ** -7 and float(diff.mean()) <= 1e-4
+    # each lse is within 2^-9 of the exact value (bf16-rounded weights, whose
+    # rounding depends on the running max and so on the split)
+    assert float((l1 - l2).abs().max()) <= 2 * 2.0 ** -9
+    rows, heads = _sample_items(inst, 600, seed=44)
+    ro, _ = oracle_lib.forward(inst, rows=rows, heads=heads)
+    sel = o2.float()[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()]
+    mx, mean = errors(sel.cpu().numpy(), ro)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
+def test_physical_permutation_is_bitwise_invariant():
+    inst = workloads.make_random(201, num_seqs=3, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                                 max_len=1500, max_segs=6, keep_logical=False, extra_blocks=5)
+    o1, l1, _ = run(DeviceInstance(inst))
+    o2, l2, _ = run(DeviceInstance(repermute(inst, 5)))
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
+def test_unreferenced_poison_and_garbage_past_context_end():
+    """NaN in blocks no table references and huge finite values past the
+    context end inside referenced blocks leave every output bit unchanged."""
+    inst = workloads.make_random(202, num_seqs=3, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                                 min_len=100, max_len=700, max_segs=4, keep_logical=False,
+                                 extra_blocks=4)
+    o1, l1, _ = run(DeviceInstance(inst))
+    bad = copy.copy(inst)
+    bad.k_cache = inst.k_cache.copy()
+    bad.v_cache = inst.v_cache.copy()
+    nan = np.uint16(0x7FC0)
+    big = workloads.f32_to_bf16_bits(np.float32(1e30))
+    used = set(int(x) for x in inst.block_table[inst.block_table >= 0].ravel())
+    for blk in range(inst.num_blocks):
+        if blk not in used:
+            bad.k_cache[blk] = nan
+            bad.v_cache[blk] = nan
+    for b in range(inst.num_seqs):
+        L = int(inst.seq_kv_len[b])
+        if L % 16:
+            blk = inst.block_table[b, L // 16]
+            bad.k_cache[blk, :, L % 16:, :] = big
+            bad.v_cache[blk, :, :, L % 16:] = big
+    o2, l2, _ = run(DeviceInstance(bad))
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
+def test_strided_output_guard_rows_untouched(oracle_lib):
+    """o written through non-contiguous strides; the gaps and guard rows
+    around the output stay exactly as they were."""
+    inst = workloads.make_random(203, num_seqs=2, num_q_heads=8, num_kv_heads=2, head_dim=64,
+                                 max_len=600, max_segs=4, keep_logical=False)
+    d = DeviceInstance(inst)
+    T, Hq, D = inst.total_q, inst.num_q_heads, inst.head_dim
+    tok_stride, head_stride = (Hq + 1) * D + 8, D + 8
+    buf = torch.full((T + 2, tok_stride), 7.0, dtype=torch.bfloat16, device="cuda")
+    base = buf[1:]
+    plan = d.plan(o_strides=(tok_stride, head_stride))
+    msa.msa_forward(plan, d.q, d.k, d.v, d.bt, base, None, None)
+    torch.cuda.synchronize()
+    host = buf.float().cpu().numpy()
+    assert (host[0] == 7.0).all() and (host[-1] == 7.0).all()
+    rows = host[1:T + 1]
+    o = np.stack([rows[:, h * head_stride: h * head_stride + D] for h in range(Hq)], axis=1)
+    mask = np.ones(tok_stride, bool)
+    for h in range(Hq):
+        mask[h * head_stride: h * head_stride + D] = False
+    assert (rows[:, mask] == 7.0).all()
+    ro, _ = oracle_lib.forward(inst)
+    mx, mean = errors(o, ro)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
+def test_block_ids_past_2gib_offsets(oracle_lib):
+    """Physical block ids whose element offsets exceed 2^31: addressing must
+    be 64-bit.  The cache is ~4.3 GB per tensor; the referenced blocks sit at
+    its top."""
+    inst = workloads.make_random(204, num_seqs=2, num_q_heads=16, num_kv_heads=8, head_dim=128,
+                                 min_len=200, max_len=500, max_segs=3, keep_logical=False)
+    per_block = inst.num_kv_heads * 16 * inst.head_dim       # elements per block
+    top = (2 ** 31) // per_block + 64 + inst.num_blocks      # blocks in the big cache
+    off = top - inst.num_blocks
+    assert off * per_block > 2 ** 31
+    k = torch.zeros((top, inst.num_kv_heads, 16, inst.head_dim), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros((top, inst.num_kv_heads, inst.head_dim, 16), dtype=torch.bfloat16, device="cuda")
+    k[off:] = dev_bf16(inst.k_cache)
+    v[off:] = dev_bf16(inst.v_cache)
+    bt = inst.block_table.copy()
+    bt[bt >= 0] += off
+    btd = torch.from_numpy(bt).cuda()
+    shape = msa.make_shape(inst.num_seqs, inst.num_q_heads, inst.num_kv_heads, inst.head_dim,
+                           inst.max_blocks_per_seq, top, inst.scale)
+    plan = msa.msa_plan(shape, inst.seq_kv_len, inst.seg_indptr, inst.seg_start, inst.seg_len)
+    q = dev_bf16(inst.q)
+    o = torch.full((inst.total_q, inst.num_q_heads, inst.head_dim), float("nan"),
+                   dtype=torch.bfloat16, device="cuda")
+    msa.msa_forward(plan, q, k, v, btd, o, None, None)
+    torch.cuda.synchronize()
+    del k, v
+    ro, _ = oracle_lib.forward(inst)
+    mx, mean = errors(bf16_to_f32(o), ro)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
+def test_forward_argument_errors():
+    inst = workloads.make_config(1)
+    d = DeviceInstance(inst)
+    plan = d.plan(kv_split_tokens=128)
+    need = plan.info()["workspace_bytes"]
+    assert need > 0
+    o = torch.empty((inst.total_q, inst.num_q_heads, inst.head_dim), dtype=torch.bfloat16,
+                    device="cuda")
+    small = torch.empty(need - 16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(msa.MsaError) as e:
+        msa.msa_forward(plan, d.q, d.k, d.v, d.bt, o, None, small)
+    assert e.value.status == msa.MSA_ERR_INVALID_ARG and "workspace" in msa.msa_last_error()
+    with pytest.raises(msa.MsaError):
+        msa.msa_forward(plan, d.q, d.k, d.v, d.bt, None, None, None)
+    raw = torch.empty(o.numel() * 2 + 8, dtype=torch.uint8, device="cuda")
+    with pytest.raises(msa.MsaError):   # misaligned output pointer
+        msa.msa_forward(plan, d.q, d.k, d.v, d.bt, raw.data_ptr() + 2, None, None)
+
+
+def test_plan_reuse_across_layers_and_streams(oracle_lib):
+    """One plan, several 'layers' (different K/V caches) and two streams."""
+    inst = workloads.make_random(205, num_seqs=2, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                                 max_len=800, max_segs=4, keep_logical=False)
+    other = workloads.make_random(205, num_seqs=2, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                                  max_len=800, max_segs=4, keep_logical=False)
+    rng = np.random.Generator(np.random.PCG64(9))
+    other.k_cache = workloads.f32_to_bf16_bits(rng.standard_normal(inst.k_cache.shape, np.float32))
+    d1, d2 = DeviceInstance(inst), DeviceInstance(other)
+    plan = d1.plan()
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for dd, s in ((d1, s1), (d2, s2)):
+        o = torch.empty((inst.total_q, inst.num_q_heads, inst.head_dim), dtype=torch.bfloat16,
+                        device="cuda")
+        msa.msa_forward(plan, dd.q, dd.k, dd.v, dd.bt, o, None, None, stream=s)
+        outs.append(o)
+    torch.cuda.synchronize()
+    for o, ii in zip(outs, (inst, other)):
+        ro, _ = oracle_lib.forward(ii)
+        mx, mean = errors(bf16_to_f32(o), ro)
+        assert mx <= MAX_ABS and mean <= MEAN_ABS
