@@ -82,7 +82,7 @@ typedef struct msa_shape {
   int32_t block_size;         /* bs: 16 */
   int32_t max_blocks_per_seq; /* row stride of block_table (entries) */
   int32_t num_blocks;         /* physical blocks in each cache */
-  float scale;                /* softmax scale, 1/sqrt(d) in the paper's Eq. 1 */
+  float scale;                /* softmax scale > 0, 1/sqrt(d) in the paper's Eq. 1 */
   int64_t q_stride_tok, q_stride_head;                 /* channel stride is 1 */
   int64_t o_stride_tok, o_stride_head;                 /* channel stride is 1 */
   int64_t k_stride_block, k_stride_head, k_stride_tok; /* channel stride is 1 */

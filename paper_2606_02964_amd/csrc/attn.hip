@@ -12,7 +12,11 @@
 //   - per-row causal limit: key j is visible to the row at absolute position
 //     p iff j <= p (applied only on steps that reach past the smallest
 //     position of the wave);
-//   - online softmax in fp32 (exp2 domain, scale * log2(e) folded in);
+//   - online softmax in fp32 in the exp2 domain: the row max is taken on the
+//     raw scores, scale * log2(e) enters one FMA per score; the reference max
+//     only moves (and O is only rescaled) when a row's max grows by more than
+//     2^8, so most steps skip the rescale; the row sum adds the bf16-rounded
+//     weights with v_dot2 against (1, 1);
 //   - O^T += V^T P^T on the same MFMA: P is the B operand and is packed to
 //     bf16 straight from the score registers.  The A-operand row order of K is
 //     permuted (bits 2 and 3 of the row index swapped) so that the 8 scores a
@@ -23,6 +27,7 @@
 
 #include <climits>
 #include <cstdint>
+#include <type_traits>
 
 #include "msa_internal.h"
 
@@ -31,6 +36,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -60,6 +66,17 @@ __device__ __forceinline__ float pair_sum(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
+
+// bf16 pair (a, b) packed into one register, round to nearest even
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  const bf16x2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// running-max threshold of the lazy rescale: the reference max only moves
+// when a row's max grows by more than this (log2 units), so the unnormalised
+// weights stay <= 2^8
+constexpr float kRescaleLog2 = 8.0f;
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
@@ -102,29 +119,46 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
     }
   }
 
+  // Gather geometry.  One cache block of one KV head is 16 keys x D
+  // channels = 2*D chunks of 16 bytes per tensor; 256 threads cover
+  // 256 / (2*D) blocks per round, kRounds rounds cover the 4 blocks of a
+  // step.  Thread tid takes chunk cb = tid % (2*D) of block
+  // i * (256 / (2*D)) + tid / (2*D) in round i.
+  constexpr int kChunksPerBlock = 2 * D;
+  constexpr int kBlocksPerRound = 256 / kChunksPerBlock;
+  const int cb = tid % kChunksPerBlock;
+  const int bsub = tid / kChunksPerBlock;  // wave-uniform
+  const int kkey = cb / (D / 8), kdch = cb % (D / 8);
+  const int vch = cb >> 1, vhalf = cb & 1;
+  const uint32_t koff = (uint32_t)(kkey * p.k_st + kdch * 8) * 2u;   // bytes inside a block
+  const uint32_t voff = (uint32_t)(vch * p.v_sd + vhalf * 8) * 2u;
+  const int64_t ksb = p.k_sb * 2, vsb = p.v_sb * 2;                   // bytes per block
+  const char* kbase = reinterpret_cast<const char*>(p.k + (int64_t)w.kv_head * p.k_sh);
+  const char* vbase = reinterpret_cast<const char*>(p.v + (int64_t)w.kv_head * p.v_sh);
   const int32_t* bt = p.block_table + (int64_t)w.seq * p.max_blocks;
-  const uint16_t* kbase = p.k + (int64_t)w.kv_head * p.k_sh;
-  const uint16_t* vbase = p.v + (int64_t)w.kv_head * p.v_sh;
+  int klds[T::kRounds], vlds[T::kRounds];
+#pragma unroll
+  for (int i = 0; i < T::kRounds; ++i) {
+    const int blk = i * kBlocksPerRound + bsub;
+    klds[i] = (blk * 16 + kkey) * T::kPitchK + kdch * 16;
+    vlds[i] = T::kBytesK + vch * T::kPitchV + (blk * 16 + vhalf * 8) * 2;
+  }
 
   uint4 kr[T::kRounds], vr[T::kRounds];
   // global -> registers for the step starting at key kb; blocks at or past
   // kv_hi are not read (their block-table entries need not be valid)
   auto load = [&](int kb) {
+    int ids[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ids[j] = kb + j * kBlockSize < w.kv_hi ? bt[(kb >> 4) + j] : -1;
 #pragma unroll
     for (int i = 0; i < T::kRounds; ++i) {
-      const int c = tid + 256 * i;
-      const int key = c / (D / 8), dch = c % (D / 8), page = key >> 4;
-      if (kb + page * kBlockSize < w.kv_hi) {
-        const int64_t blk = bt[(kb >> 4) + page];
-        kr[i] = *reinterpret_cast<const uint4*>(kbase + blk * p.k_sb + (key & 15) * p.k_st + dch * 8);
+      const int id = kBlocksPerRound == 1 ? ids[i] : ids[i * kBlocksPerRound + bsub];
+      if (id >= 0) {
+        kr[i] = *reinterpret_cast<const uint4*>(kbase + id * ksb + koff);
+        vr[i] = *reinterpret_cast<const uint4*>(vbase + id * vsb + voff);
       } else {
         kr[i] = make_uint4(0, 0, 0, 0);
-      }
-      const int vpage = c / (2 * D), rem = c % (2 * D), ch = rem >> 1, half = rem & 1;
-      if (kb + vpage * kBlockSize < w.kv_hi) {
-        const int64_t blk = bt[(kb >> 4) + vpage];
-        vr[i] = *reinterpret_cast<const uint4*>(vbase + blk * p.v_sb + ch * p.v_sd + half * 8);
-      } else {
         vr[i] = make_uint4(0, 0, 0, 0);
       }
     }
@@ -132,20 +166,95 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
   auto store = [&](char* st) {
 #pragma unroll
     for (int i = 0; i < T::kRounds; ++i) {
-      const int c = tid + 256 * i;
-      const int key = c / (D / 8), dch = c % (D / 8);
-      *reinterpret_cast<uint4*>(st + key * T::kPitchK + dch * 16) = kr[i];
-      const int vpage = c / (2 * D), rem = c % (2 * D), ch = rem >> 1, half = rem & 1;
-      *reinterpret_cast<uint4*>(st + T::kBytesK + ch * T::kPitchV + (vpage * 16 + half * 8) * 2) = vr[i];
+      *reinterpret_cast<uint4*>(st + klds[i]) = kr[i];
+      *reinterpret_cast<uint4*>(st + vlds[i]) = vr[i];
     }
   };
 
-  float m_run = -__builtin_inff(), l_run = 0.0f;
+  const float c = p.scale_log2;  // > 0
+  float m_ref = -__builtin_inff(), l_run = 0.0f;
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.0f;
+  const int klane = swap_bits23(ln) * T::kPitchK + hl * 16;
+  const int vlane = T::kBytesK + ln * T::kPitchV + hl * 16;
+
+  // one 64-key step over the LDS stage `cur`
+  auto step = [&](const char* cur, int kb, auto masked) {
+    constexpr bool kMasked = decltype(masked)::value;
+    // S^T = K Q^T: two 32-key tiles
+    f32x16 s[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const char* krow = cur + kt * 32 * T::kPitchK + klane;
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + kk * 32);
+        if (kk == 0) {
+          const f32x16 zero = {};
+          s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0], zero, 0, 0, 0);
+        } else {
+          s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[kt], 0, 0, 0);
+        }
+      }
+    }
+    // lane (hl, ln), register i of tile kt holds key kb + kt*32 + (i/8)*16 + hl*8 + i%8
+    if constexpr (kMasked) {
+      const int lim = pos - kb - hl * 8;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          s[kt][i] = (kt * 32 + (i >> 3) * 16 + (i & 7)) <= lim ? s[kt][i] : -__builtin_inff();
+    }
+    float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+    for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[0][i]);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[1][i]);
+    const float m_blk = pair_max(mx) * c;
+    const bool grow = m_blk > m_ref + kRescaleLog2;
+    if (__any(grow)) {  // wave-uniform
+      const float alpha = grow ? __builtin_amdgcn_exp2f(m_ref - m_blk) : 1.0f;
+      m_ref = grow ? m_blk : m_ref;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+    }
+    // a row with no visible key so far keeps m_ref = -inf; its scores are -inf too
+    const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
+    uint32_t pk[2][8];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 16; i += 2)
+        pk[kt][i >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][i], c, nm)),
+                                     __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][i + 1], c, nm)));
+    // the row sum adds the same bf16-rounded weights that enter the PV
+    // product, so the normalised weights sum to one exactly
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    float ls = 0.0f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][j]), ones, ls, false);
+    l_run += ls;
+    // O^T += V^T P^T: 4 steps of 16 keys; step ks takes keys 16*ks + hl*8 .. +8
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 u = make_uint4(pk[ks >> 1][(ks & 1) * 4 + 0], pk[ks >> 1][(ks & 1) * 4 + 1],
+                                 pk[ks >> 1][(ks & 1) * 4 + 2], pk[ks >> 1][(ks & 1) * 4 + 3]);
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, u);
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(cur + vlane + dt * 32 * T::kPitchV + ks * 32);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
+      }
+    }
+  };
 
   const int nsteps = (w.kv_hi - w.kv_lo + kKvStep - 1) / kKvStep;
   load(w.kv_lo);
@@ -158,69 +267,12 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
     char* nxt = smem + ((it + 1) & 1) * T::kStage;
     const bool more = it + 1 < nsteps;
     if (more) load(kb + kKvStep);
-
     if (kb <= pmax) {  // some row of this wave sees a key of this step
-      // S^T = K Q^T: two 32-key tiles
-      f32x16 s[2];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) s[kt][i] = 0.0f;
-        const char* krow = cur + (kt * 32 + swap_bits23(ln)) * T::kPitchK + hl * 16;
-#pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + kk * 32);
-          s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[kt], 0, 0, 0);
-        }
-      }
-      // lane (hl, ln), register i of tile kt holds key kb + kt*32 + (i/8)*16 + hl*8 + i%8
-      const bool need_mask = kb + kKvStep - 1 > pmin;
-      float mx = -__builtin_inff();
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float x = s[kt][i] * p.scale_log2;
-          if (need_mask) {
-            const int key = kb + kt * 32 + (i >> 3) * 16 + hl * 8 + (i & 7);
-            x = key <= pos ? x : -__builtin_inff();
-          }
-          s[kt][i] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = pair_max(mx);
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = m_new == -__builtin_inff() ? 0.0f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-      // P is rounded to bf16 for the PV product; the row sum adds the same
-      // rounded values, so the normalised weights sum to one exactly and the
-      // output stays a convex combination of the values
-      float ls = 0.0f;
-      bf16x8 pb[4];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const __bf16 e = (__bf16)__builtin_amdgcn_exp2f(s[kt][i] - m_use);
-          ls += (float)e;
-          pb[kt * 2 + (i >> 3)][i & 7] = e;
-        }
-      l_run = l_run * alpha + ls;
-      m_run = m_new;
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
-      // O^T += V^T P^T: 4 steps of 16 keys
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        const char* vrow = cur + T::kBytesK + (dt * 32 + ln) * T::kPitchV + hl * 16;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(vrow + ks * 32);
-          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[dt], 0, 0, 0);
-        }
-      }
+      if (kb + kKvStep - 1 > pmin)
+        step(cur, kb, std::true_type{});
+      else
+        step(cur, kb, std::false_type{});
     }
-
     if (more) store(nxt);
     __syncthreads();
   }
@@ -235,13 +287,12 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        bf16x4 v;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = (__bf16)(oacc[dt][g4 * 4 + j] * inv);
-        *reinterpret_cast<bf16x4*>(orow + dt * 32 + g4 * 8 + hl * 4) = v;
+        const uint2 v = make_uint2(pack_bf16x2(oacc[dt][g4 * 4 + 0] * inv, oacc[dt][g4 * 4 + 1] * inv),
+                                   pack_bf16x2(oacc[dt][g4 * 4 + 2] * inv, oacc[dt][g4 * 4 + 3] * inv));
+        *reinterpret_cast<uint2*>(orow + dt * 32 + g4 * 8 + hl * 4) = v;
       }
     if (p.lse && hl == 0)
-      p.lse[(int64_t)tok * p.num_q_heads + head] = (m_run + __log2f(l_tot)) * kLn2;
+      p.lse[(int64_t)tok * p.num_q_heads + head] = (m_ref + __log2f(l_tot)) * kLn2;
   } else {
     float* slot = p.ws + (int64_t)w.out_slot * kTileRows * (D + 1);
     const bool empty = !(l_tot > 0.0f);  // no visible key in this split
@@ -257,7 +308,7 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
         *reinterpret_cast<f32x4*>(orow + dt * 32 + g4 * 8 + hl * 4) = v;
       }
     if (hl == 0)
-      slot[kTileRows * D + r] = empty ? -__builtin_inff() : (m_run + __log2f(l_tot)) * kLn2;
+      slot[kTileRows * D + r] = empty ? -__builtin_inff() : (m_ref + __log2f(l_tot)) * kLn2;
   }
 }
 

@@ -70,7 +70,8 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   if (s.block_size != kBlockSize) return fail(err, MSA_ERR_UNSUPPORTED, "block_size must be 16");
   if (s.max_blocks_per_seq < 0 || s.num_blocks < 0)
     return fail(err, MSA_ERR_INVALID_ARG, "max_blocks_per_seq and num_blocks must be >= 0");
-  if (!std::isfinite(s.scale)) return fail(err, MSA_ERR_INVALID_ARG, "scale must be finite");
+  if (!std::isfinite(s.scale) || !(s.scale > 0.0f))
+    return fail(err, MSA_ERR_INVALID_ARG, "scale must be finite and > 0");
   if (!aligned8(s.q_stride_tok) || !aligned8(s.q_stride_head) || !aligned8(s.o_stride_tok) ||
       !aligned8(s.o_stride_head) || !aligned8(s.k_stride_block) || !aligned8(s.k_stride_head) ||
       !aligned8(s.k_stride_tok) || !aligned8(s.v_stride_block) || !aligned8(s.v_stride_head) ||

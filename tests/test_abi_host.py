@@ -266,7 +266,8 @@ def test_plan_rejects_malformed_segments(msa, what):
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 96, 2), ("head_dim", 0, 1), ("block_size", 32, 2), ("block_size", 0, 1),
     ("num_kv_heads", 3, 1), ("num_q_heads", 0, 1), ("q_stride_tok", 12, 1),
-    ("v_stride_dim", 0, 1), ("scale", float("nan"), 1), ("num_seqs", -1, 1)])
+    ("v_stride_dim", 0, 1), ("scale", float("nan"), 1), ("scale", 0.0, 1), ("scale", -0.5, 1),
+    ("num_seqs", -1, 1)])
 def test_plan_rejects_bad_shapes(msa, field, value, status):
     inst = workloads.make_layout(8, [256], [[(10, 30)]], 4, 2, 64)
     sh = shape_of(msa, inst)
