@@ -106,12 +106,13 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (2 = Llama-8B shape)")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--no-cold", action="store_true", help="skip the cache-flushed timing")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time calls after flushing L2 and the infinity cache (extra launches)")
     ap.add_argument("--kv-split-tokens", type=int, default=0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES bytes (HBM counter calibration)")
@@ -173,7 +174,7 @@ def main():
     log(f"warm: {ms * 1e3:.1f} us/call")
 
     cold_ms = None
-    if not args.no_cold:
+    if args.cold:
         flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
         times = []
         for _ in range(max(3, min(args.steps, 10))):
