@@ -7,7 +7,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/msa.h"
+#include "msa.h"
 #include "msa_internal.h"
 #include "plan.h"
 

@@ -4,7 +4,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/msa.h"
+#include "msa.h"
 #include "msa_internal.h"
 
 namespace msa {
