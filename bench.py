@@ -102,6 +102,83 @@ def calibrate_copy(nbytes: int, reps: int):
     print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "reps": reps}))
 
 
+def time_calls(step, stream, warmup, steps):
+    """Mean milliseconds per call over `steps` calls after `warmup` calls."""
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        step()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
+REPORT_CASES = [
+    # (label, workload, make_config keyword arguments)
+    ("tiny", 1, {}),
+    ("llama8b", 2, {}),
+    ("fragmented", 3, {}),
+    ("long70b", 4, {}),
+    ("long70b-tp4-rank (16q/2kv)", 4, {"num_q_heads": 16, "num_kv_heads": 2}),
+    ("mixed", 5, {}),
+    ("mixed-decode-only", 5, {"decode_only": True}),
+]
+
+
+def report_all(path: str, steps: int, warmup: int):
+    """Time every named workload (plus two supplementary shapes) and write
+    one JSON line per case to `path`."""
+    import numpy as np
+    import torch
+    import workloads
+    import paper_2606_02964_amd as msa
+
+    def dev_bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    stream = torch.cuda.current_stream()
+    with open(path, "w") as out:
+        for label, cfg, kw in REPORT_CASES:
+            inst = workloads.make_config(cfg, **kw)
+            q, k, v = dev_bf16(inst.q), dev_bf16(inst.k_cache), dev_bf16(inst.v_cache)
+            bt = torch.from_numpy(np.ascontiguousarray(inst.block_table)).cuda()
+            shape = msa.make_shape(inst.num_seqs, inst.num_q_heads, inst.num_kv_heads, inst.head_dim,
+                                   inst.max_blocks_per_seq, inst.num_blocks, inst.scale)
+            plan = msa.msa_plan(shape, inst.seq_kv_len, inst.seg_indptr, inst.seg_start, inst.seg_len,
+                                stream=stream)
+            info = plan.info()
+            o = torch.empty((inst.total_q, inst.num_q_heads, inst.head_dim), dtype=torch.bfloat16,
+                            device="cuda")
+            ws = (torch.empty(info["workspace_bytes"], dtype=torch.uint8, device="cuda")
+                  if info["workspace_bytes"] else None)
+            ms = time_calls(lambda: msa.msa_forward(plan, q, k, v, bt, o, None, ws, stream=stream),
+                            stream, warmup, steps)
+            t = ms * 1e-3
+            rec = {
+                "case": label,
+                "workload": workloads.CONFIG_DESCRIPTIONS[cfg] + (f" {kw}" if kw else ""),
+                "q_rows": inst.total_q, "segments": int(len(inst.seg_len)),
+                "us_per_call": round(ms * 1e3, 1),
+                "useful_tflops": round(info["useful_flops"] / t / 1e12, 2),
+                "frac_mfma": round(info["useful_flops"] / t / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "min_bytes_gbs": round(info["min_bytes"] / t / 1e9, 1),
+                "frac_hbm_min_bytes": round(info["min_bytes"] / t / 1e9 / PEAK_HBM_GBS, 4),
+                "planned_bytes_gbs": round(info["planned_bytes"] / t / 1e9, 1),
+                "tile_flop_ratio": round(info["tile_flops"] / max(info["useful_flops"], 1.0), 4),
+                "work_items": info["num_work"], "split_tiles": info["num_merge"],
+                "max_splits": info["max_splits"],
+            }
+            out.write(json.dumps(rec) + "\n")
+            out.flush()
+            log(f"report: {rec}")
+            del q, k, v, bt, o, ws, plan
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -114,6 +191,8 @@ def main():
     ap.add_argument("--cold", action="store_true",
                     help="also time calls after flushing L2 and the infinity cache (extra launches)")
     ap.add_argument("--kv-split-tokens", type=int, default=0)
+    ap.add_argument("--report", metavar="PATH", default=None,
+                    help="only time every named workload and write one JSON line per case to PATH")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES bytes (HBM counter calibration)")
     args = ap.parse_args()
@@ -130,6 +209,9 @@ def main():
         sys.exit(1)
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy, max(1, args.steps))
+        return
+    if args.report:
+        report_all(args.report, args.steps, args.warmup)
         return
 
     import workloads

@@ -268,11 +268,21 @@ CONFIG_DESCRIPTIONS = {
 
 
 def make_config(cfg: int, seed: Optional[int] = None, keep_logical: bool = False,
-                **layout_kw) -> Instance:
-    """Instance of named workload ``cfg`` (1..5).  Default seed = cfg."""
+                decode_only: bool = False, **layout_kw) -> Instance:
+    """Instance of named workload ``cfg`` (1..5).  Default seed = cfg.
+
+    ``decode_only`` keeps just the sequences whose only segment is their last
+    token (the decode rows of the mixed workload) with the same context
+    lengths; their values are drawn afresh.
+    """
     name, layout = CONFIGS[cfg]
     rng = np.random.Generator(np.random.PCG64(cfg if seed is None else seed))
     lens, segs, heads = layout(rng, **layout_kw)
+    if decode_only:
+        keep = [b for b in range(len(lens)) if segs[b] == [(lens[b] - 1, 1)]]
+        lens = [lens[b] for b in keep]
+        segs = [segs[b] for b in keep]
+        name += "-decode"
     return build_instance(name, rng, lens, segs, keep_logical=keep_logical, **heads)
 
 
