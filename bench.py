@@ -158,6 +158,11 @@ def report_all(path: str, steps: int, warmup: int):
             ms = time_calls(lambda: msa.msa_forward(plan, q, k, v, bt, o, None, ws, stream=stream),
                             stream, warmup, steps)
             t = ms * 1e-3
+            # the layer's cache write of the same rows (fresh K/V into the paged cache)
+            kn, vn = (dev_bf16(x) for x in workloads.make_fresh_kv(inst, 4242))
+            ms_app = time_calls(lambda: msa.msa_kv_append(plan, kn, vn, bt, k, v, stream=stream),
+                                stream, warmup, steps)
+            app_bytes = 4.0 * inst.total_q * inst.num_kv_heads * inst.head_dim * 2
             rec = {
                 "case": label,
                 "workload": workloads.CONFIG_DESCRIPTIONS[cfg] + (f" {kw}" if kw else ""),
@@ -171,11 +176,14 @@ def report_all(path: str, steps: int, warmup: int):
                 "tile_flop_ratio": round(info["tile_flops"] / max(info["useful_flops"], 1.0), 4),
                 "work_items": info["num_work"], "split_tiles": info["num_merge"],
                 "max_splits": info["max_splits"],
+                "append_us_per_call": round(ms_app * 1e3, 2),
+                "append_gbs": round(app_bytes / (ms_app * 1e-3) / 1e9, 1),
+                "append_frac_hbm": round(app_bytes / (ms_app * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             }
             out.write(json.dumps(rec) + "\n")
             out.flush()
             log(f"report: {rec}")
-            del q, k, v, bt, o, ws, plan
+            del q, k, v, bt, o, ws, plan, kn, vn
             torch.cuda.empty_cache()
 
 

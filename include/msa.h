@@ -167,6 +167,39 @@ msa_status msa_forward(msa_plan_t plan, const void *q, const void *k_cache, cons
                        const int32_t *block_table, void *o, float *lse, void *workspace,
                        size_t workspace_bytes, void *hip_stream);
 
+/*
+ * msa_kv_append: write the fresh keys and values of every packed query row
+ * into the paged cache, at the row's absolute position.  All segments'
+ * tokens go through one forward pass (Sec. 4.1), so each layer produces K/V
+ * for every packed row; they must sit in the PagedAttention-style cache
+ * (Sec. 5.3) before msa_forward reads them (K/V of earlier segments are
+ * keys of later ones).  Same plan, same row order as msa_forward.
+ *
+ *   k_new, v_new  device bf16 [total_q, Hkv, d]: element (r, g, c) at
+ *                 k_new + r*k_new_stride_tok + g*k_new_stride_head + c
+ *                 (likewise v_new with its own strides; channel stride 1;
+ *                 strides in elements, positive multiples of 8)
+ *   block_table   device int32 [num_seqs * max_blocks_per_seq]
+ *   k_cache, v_cache  device caches in the layout of the conventions above
+ *   hip_stream    hipStream_t on which the kernel is enqueued (no host sync)
+ *
+ * Row r (sequence b, position p) writes K[blk, g, p % 16, :] and
+ * V[blk, g, :, p % 16] for every kv head g, blk = block_table[b][p / 16].
+ * Nothing else in the caches is written.  A row whose block-table entry is
+ * outside [0, num_blocks) is skipped (not written).  No two rows may map to
+ * the same cache slot (e.g. through physical blocks shared by sequences):
+ * such writes race.  The new K/V must not overlap the caches.
+ *
+ * Returns MSA_ERR_INVALID_ARG for NULL or misaligned pointers, bad strides
+ * or a host-only plan; MSA_ERR_DEVICE if the launch fails.  A plan with no
+ * rows returns MSA_OK and launches nothing.
+ */
+msa_status msa_kv_append(msa_plan_t plan, const void *k_new, const void *v_new,
+                         int64_t k_new_stride_tok, int64_t k_new_stride_head,
+                         int64_t v_new_stride_tok, int64_t v_new_stride_head,
+                         const int32_t *block_table, void *k_cache, void *v_cache,
+                         void *hip_stream);
+
 /* msa_plan_destroy: free a plan.  The caller must have synchronised every
  * stream that used it.  NULL is accepted. */
 void msa_plan_destroy(msa_plan_t plan);

@@ -4,6 +4,7 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline
 leg may import this package.  The product (``paper_2606_02964_amd``) never
 does, and this package never imports the product.
 
+``kv_append`` is the paged cache write of the rows' fresh K/V (Sec. 4.1, 5.3).
 ``forward`` is exact MSA (Sec. 2.1 Eq. 1 + Sec. 4.1 Eq. 2, causal by absolute
 position, GQA grouping h -> h / (Hq/Hkv)), computed in IEEE double by the
 plain C routine in ``msa_oracle.c``.
@@ -62,6 +63,15 @@ def _declare(lib):
         P,                                       # block table
         P, P, i64,                               # items
         P, P, i32]                               # outputs, threads
+    lib.msa_oracle_kv_append.restype = ctypes.c_int
+    lib.msa_oracle_kv_append.argtypes = [
+        i32, i32, i32, i32, i32, i32,            # shapes
+        P, P, P, P,                              # seq_kv_len, seg_indptr, seg_start, seg_len
+        P, i64, i64,                             # k_new
+        P, i64, i64,                             # v_new
+        P, i64, i64, i64,                        # k cache (written)
+        P, i64, i64, i64,                        # v cache (written)
+        P]                                       # block table
     lib.msa_oracle_total_rows.restype = i64
     lib.msa_oracle_total_rows.argtypes = [i32, P, P]
 
@@ -124,3 +134,33 @@ def forward(inst, rows: Optional[np.ndarray] = None, heads: Optional[np.ndarray]
     if rc != 0:
         raise ValueError(f"msa_oracle_forward rejected its inputs (code {rc})")
     return o, lse
+
+
+def kv_append(inst, k_new: np.ndarray, v_new: np.ndarray, lib=None) -> Tuple[np.ndarray, np.ndarray]:
+    """Paged cache write of the rows' K/V: returns copies of ``inst``'s caches
+    with k_new / v_new ([total_q, Hkv, d] bf16 bits) stored at every row's
+    absolute position.  ``inst``'s own caches are not modified."""
+    lib = _load() if lib is None else lib
+    c = np.ascontiguousarray
+    seq_kv_len = c(inst.seq_kv_len, dtype=np.int32)
+    seg_indptr = c(inst.seg_indptr, dtype=np.int32)
+    seg_start = c(inst.seg_start, dtype=np.int32)
+    seg_len = c(inst.seg_len, dtype=np.int32)
+    kn = c(k_new, dtype=np.uint16)
+    vn = c(v_new, dtype=np.uint16)
+    k = np.array(inst.k_cache, dtype=np.uint16, copy=True, order="C")
+    v = np.array(inst.v_cache, dtype=np.uint16, copy=True, order="C")
+    bt = c(inst.block_table, dtype=np.int32)
+    Hkv, d = inst.num_kv_heads, inst.head_dim
+    total = int(seg_len.sum())
+    assert kn.shape == (total, Hkv, d) and vn.shape == (total, Hkv, d)
+    rc = lib.msa_oracle_kv_append(
+        inst.num_seqs, Hkv, d, inst.block_size, bt.shape[1], k.shape[0],
+        _ptr(seq_kv_len), _ptr(seg_indptr), _ptr(seg_start), _ptr(seg_len),
+        _ptr(kn), Hkv * d, d, _ptr(vn), Hkv * d, d,
+        _ptr(k), Hkv * k.shape[2] * d, k.shape[2] * d, d,
+        _ptr(v), Hkv * d * v.shape[3], d * v.shape[3], v.shape[3],
+        _ptr(bt))
+    if rc != 0:
+        raise ValueError(f"msa_oracle_kv_append rejected its inputs (code {rc})")
+    return k, v

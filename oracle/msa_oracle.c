@@ -285,3 +285,56 @@ int msa_oracle_forward(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_hea
   free(row_pos);
   return failed ? MSA_ORACLE_NO_MEM : MSA_ORACLE_OK;
 }
+
+/*
+ * msa_oracle_kv_append: the cache write that precedes attention.  All
+ * segments' tokens go through one forward pass (Sec. 4.1), which yields the
+ * key and value of every packed row; each is stored in the paged cache
+ * (Sec. 5.3, PagedAttention's block table) at the row's absolute position:
+ *   K[blk, g, p % bs, c] = k_new[r, g, c],  V[blk, g, c, p % bs] = v_new[r, g, c]
+ *   for every kv head g and channel c, blk = block_table[b][p / bs].
+ * A row whose block-table entry is outside [0, num_blocks) has no slot and
+ * writes nothing.  Rows are written in packed order.  Returns 0, or a nonzero
+ * code (nothing written) when the segments break the layout's rules.
+ */
+int msa_oracle_kv_append(int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
+                         int32_t block_size, int32_t max_blocks_per_seq, int32_t num_blocks,
+                         const int32_t *seq_kv_len, const int32_t *seg_indptr,
+                         const int32_t *seg_start, const int32_t *seg_len,
+                         const uint16_t *k_new, int64_t kn_stride_tok, int64_t kn_stride_head,
+                         const uint16_t *v_new, int64_t vn_stride_tok, int64_t vn_stride_head,
+                         uint16_t *k_cache, int64_t k_stride_block, int64_t k_stride_head,
+                         int64_t k_stride_tok, uint16_t *v_cache, int64_t v_stride_block,
+                         int64_t v_stride_head, int64_t v_stride_dim,
+                         const int32_t *block_table) {
+  if (num_seqs < 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return MSA_ORACLE_BAD_ARG;
+  /* the same segment rules as the attention */
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    int32_t prev_end = 0;
+    for (int32_t s = seg_indptr[b]; s < seg_indptr[b + 1]; ++s) {
+      if (seg_len[s] < 1 || seg_start[s] < prev_end ||
+          (int64_t)seg_start[s] + seg_len[s] > seq_kv_len[b] ||
+          (int64_t)seq_kv_len[b] > (int64_t)max_blocks_per_seq * block_size)
+        return MSA_ORACLE_BAD_ARG;
+      prev_end = seg_start[s] + seg_len[s];
+    }
+  }
+  int64_t r = 0;
+  for (int32_t b = 0; b < num_seqs; ++b)
+    for (int32_t s = seg_indptr[b]; s < seg_indptr[b + 1]; ++s)
+      for (int32_t t = 0; t < seg_len[s]; ++t, ++r) {
+        const int32_t p = seg_start[s] + t;
+        const int32_t blk = block_table[(int64_t)b * max_blocks_per_seq + p / block_size];
+        if (blk < 0 || blk >= num_blocks) continue;
+        const int32_t off = p % block_size;
+        for (int32_t g = 0; g < num_kv_heads; ++g)
+          for (int32_t c = 0; c < head_dim; ++c) {
+            k_cache[blk * k_stride_block + g * k_stride_head + off * k_stride_tok + c] =
+                k_new[r * kn_stride_tok + g * kn_stride_head + c];
+            v_cache[blk * v_stride_block + g * v_stride_head + c * v_stride_dim + off] =
+                v_new[r * vn_stride_tok + g * vn_stride_head + c];
+          }
+      }
+  return MSA_ORACLE_OK;
+}

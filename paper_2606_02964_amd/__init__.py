@@ -6,8 +6,8 @@ step of the attention runs in the library's HIP kernels.  There is no CPU
 fallback: importing this package without a built library raises.
 
 Functions carry the C names: ``msa_plan``, ``msa_plan_info``,
-``msa_forward``, ``msa_plan_destroy``, ``msa_last_error``,
-``msa_plan_export``.  Device buffers are passed as objects with a
+``msa_forward``, ``msa_kv_append``, ``msa_plan_destroy``,
+``msa_last_error``, ``msa_plan_export``.  Device buffers are passed as objects with a
 ``data_ptr()`` method (e.g. torch tensors) or as integer addresses; streams
 as ``hipStream_t`` integers or objects with ``cuda_stream`` (torch streams).
 """
@@ -68,6 +68,8 @@ _lib.msa_plan_info.restype = _i32
 _lib.msa_plan_info.argtypes = [_P, ctypes.POINTER(msa_plan_info_t)]
 _lib.msa_forward.restype = _i32
 _lib.msa_forward.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.msa_kv_append.restype = _i32
+_lib.msa_kv_append.argtypes = [_P, _P, _P, _i64, _i64, _i64, _i64, _P, _P, _P, _P]
 _lib.msa_plan_destroy.restype = None
 _lib.msa_plan_destroy.argtypes = [_P]
 _lib.msa_last_error.restype = ctypes.c_char_p
@@ -75,8 +77,8 @@ _lib.msa_last_error.argtypes = []
 _lib.msa_plan_export.restype = _i32
 _lib.msa_plan_export.argtypes = [_P, _P, _P, _P]
 
-EXPORTED = ("msa_plan", "msa_plan_info", "msa_forward", "msa_plan_destroy", "msa_last_error",
-            "msa_plan_export")
+EXPORTED = ("msa_plan", "msa_plan_info", "msa_forward", "msa_kv_append", "msa_plan_destroy",
+            "msa_last_error", "msa_plan_export")
 
 
 class MsaError(RuntimeError):
@@ -184,6 +186,28 @@ def msa_forward(plan: Plan, q, k_cache, v_cache, block_table, o, lse=None, works
     _check(_lib.msa_forward(plan.handle, _addr(q), _addr(k_cache), _addr(v_cache),
                             _addr(block_table), _addr(o), _addr(lse), _addr(workspace),
                             int(workspace_bytes), _stream(stream)))
+
+
+def msa_kv_append(plan: Plan, k_new, v_new, block_table, k_cache, v_cache,
+                  k_new_strides=None, v_new_strides=None, stream=None) -> None:
+    """Enqueue the write of the rows' fresh K/V ([total_q, Hkv, d]) into the paged cache.
+
+    Strides (tok, head) in elements default to those of a tensor argument
+    (``.stride()``), else to the contiguous layout."""
+    def strides(x, given):
+        if given is not None:
+            return int(given[0]), int(given[1])
+        if hasattr(x, "stride"):
+            st = x.stride()
+            return int(st[0]), int(st[1])
+        sh = plan.shape
+        if sh is None:  # no plan: the library reports that
+            return 0, 0
+        return sh.num_kv_heads * sh.head_dim, sh.head_dim
+    kst, ksh = strides(k_new, k_new_strides)
+    vst, vsh = strides(v_new, v_new_strides)
+    _check(_lib.msa_kv_append(plan.handle, _addr(k_new), _addr(v_new), kst, ksh, vst, vsh,
+                              _addr(block_table), _addr(k_cache), _addr(v_cache), _stream(stream)))
 
 
 def msa_plan_destroy(plan: Plan) -> None:

@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "msa.h"
+#include "append.h"
 #include "msa_internal.h"
 #include "plan.h"
 
@@ -16,10 +17,11 @@ struct msa_plan_s {
   bool host_only = true;
   int device = -1;
   std::vector<char> staging;  // host image of the device buffer (kept alive for the async copy)
-  char* dev = nullptr;        // device buffer: row_pos | work | merge
+  char* dev = nullptr;        // device buffer: row_pos | work | merge | append
   const int32_t* d_row_pos = nullptr;
   const msa::WorkItem* d_work = nullptr;
   const msa::MergeItem* d_merge = nullptr;
+  const msa::AppendItem* d_append = nullptr;
 };
 
 namespace {
@@ -66,9 +68,11 @@ msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int
     const size_t n_row = hp.row_pos.size() * sizeof(int32_t);
     const size_t n_work = hp.work.size() * sizeof(msa::WorkItem);
     const size_t n_merge = hp.merge.size() * sizeof(msa::MergeItem);
+    const size_t n_append = hp.append.size() * sizeof(msa::AppendItem);
     const size_t off_work = align_up(n_row, 256);
     const size_t off_merge = off_work + align_up(n_work, 256);
-    const size_t bytes = std::max<size_t>(off_merge + n_merge, 256);
+    const size_t off_append = off_merge + align_up(n_merge, 256);
+    const size_t bytes = std::max<size_t>(off_append + n_append, 256);
     try {
       plan->staging.assign(bytes, 0);
     } catch (const std::bad_alloc&) {
@@ -78,6 +82,7 @@ msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int
     if (n_row) std::memcpy(plan->staging.data(), hp.row_pos.data(), n_row);
     if (n_work) std::memcpy(plan->staging.data() + off_work, hp.work.data(), n_work);
     if (n_merge) std::memcpy(plan->staging.data() + off_merge, hp.merge.data(), n_merge);
+    if (n_append) std::memcpy(plan->staging.data() + off_append, hp.append.data(), n_append);
     if (hipGetDevice(&plan->device) != hipSuccess) {
       delete plan;
       return set_error(MSA_ERR_DEVICE, "msa_plan: hipGetDevice failed");
@@ -99,6 +104,7 @@ msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int
     plan->d_row_pos = reinterpret_cast<const int32_t*>(plan->dev);
     plan->d_work = reinterpret_cast<const msa::WorkItem*>(plan->dev + off_work);
     plan->d_merge = reinterpret_cast<const msa::MergeItem*>(plan->dev + off_merge);
+    plan->d_append = reinterpret_cast<const msa::AppendItem*>(plan->dev + off_append);
   }
   *out = plan;
   return MSA_OK;
@@ -204,6 +210,58 @@ msa_status msa_forward(msa_plan_t plan, const void* q, const void* k_cache, cons
     if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string("msa_forward: merge launch failed: ") +
                                                       hipGetErrorString((hipError_t)rc));
   }
+  return MSA_OK;
+}
+
+msa_status msa_kv_append(msa_plan_t plan, const void* k_new, const void* v_new,
+                         int64_t k_new_stride_tok, int64_t k_new_stride_head,
+                         int64_t v_new_stride_tok, int64_t v_new_stride_head,
+                         const int32_t* block_table, void* k_cache, void* v_cache,
+                         void* hip_stream) {
+  if (!plan) return set_error(MSA_ERR_INVALID_ARG, "msa_kv_append: null plan");
+  auto ok_stride = [](int64_t x) { return x > 0 && x % 8 == 0; };
+  if (!ok_stride(k_new_stride_tok) || !ok_stride(k_new_stride_head) ||
+      !ok_stride(v_new_stride_tok) || !ok_stride(v_new_stride_head))
+    return set_error(MSA_ERR_INVALID_ARG,
+                     "msa_kv_append: strides must be positive multiples of 8 elements");
+  if (plan->host_only)
+    return set_error(MSA_ERR_INVALID_ARG, "msa_kv_append: plan was built with MSA_PLAN_HOST_ONLY");
+  const msa::HostPlan& hp = plan->hp;
+  const msa_shape& s = hp.shape;
+  if (hp.total_q == 0) return MSA_OK;  // no query rows: nothing to write
+  if (!k_new || !v_new || !block_table || !k_cache || !v_cache)
+    return set_error(MSA_ERR_INVALID_ARG,
+                     "msa_kv_append: k_new, v_new, block_table, k_cache, v_cache must be non-null");
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+      !aligned(block_table, 4))
+    return set_error(MSA_ERR_INVALID_ARG, "msa_kv_append: k/v pointers must be 16-byte aligned");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
+    return set_error(MSA_ERR_INVALID_ARG, "msa_kv_append: current device differs from the plan's device");
+  msa::AppendParams p{};
+  p.k_new = static_cast<const uint16_t*>(k_new);
+  p.v_new = static_cast<const uint16_t*>(v_new);
+  p.block_table = block_table;
+  p.items = plan->d_append;
+  p.k_cache = static_cast<uint16_t*>(k_cache);
+  p.v_cache = static_cast<uint16_t*>(v_cache);
+  p.kn_st = k_new_stride_tok;
+  p.kn_sh = k_new_stride_head;
+  p.vn_st = v_new_stride_tok;
+  p.vn_sh = v_new_stride_head;
+  p.k_sb = s.k_stride_block;
+  p.k_sh = s.k_stride_head;
+  p.k_st = s.k_stride_tok;
+  p.v_sb = s.v_stride_block;
+  p.v_sh = s.v_stride_head;
+  p.v_sd = s.v_stride_dim;
+  p.num_kv_heads = s.num_kv_heads;
+  p.max_blocks = s.max_blocks_per_seq;
+  p.num_blocks = s.num_blocks;
+  const int rc = msa::launch_kv_append(p, s.head_dim, (int)hp.append.size(), hip_stream);
+  if (rc != 0)
+    return set_error(MSA_ERR_DEVICE, std::string("msa_kv_append: launch failed: ") +
+                                         hipGetErrorString((hipError_t)rc));
   return MSA_OK;
 }
 

@@ -136,6 +136,21 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
       for (int32_t k = seg_indptr[b]; k < seg_indptr[b + 1]; ++k)
         for (int32_t t = 0; t < seg_len[k]; ++t) P.row_pos[(size_t)r++] = seg_start[k] + t;
   }
+  // slices of the cache write: each segment cut at cache-block boundaries
+  {
+    int64_t r = 0;
+    for (int32_t b = 0; b < B; ++b)
+      for (int32_t k = seg_indptr[b]; k < seg_indptr[b + 1]; ++k) {
+        int32_t p = seg_start[k];
+        const int32_t end = seg_start[k] + seg_len[k];
+        while (p < end) {
+          const int32_t stop = std::min(end, (p / kBlockSize + 1) * kBlockSize);
+          P.append.push_back(AppendItem{(int32_t)r, b, p, stop - p});
+          r += stop - p;
+          p = stop;
+        }
+      }
+  }
 
   // 2-3. tiles and units
   std::vector<Unit> units;

@@ -4,6 +4,7 @@
 #include <string>
 #include <vector>
 
+#include "append.h"
 #include "msa.h"
 #include "msa_internal.h"
 
@@ -14,9 +15,10 @@ struct HostPlan {
   int32_t group = 1;        // G = Hq / Hkv
   int32_t tile_tokens = 0;  // query tokens per tile
   int64_t total_q = 0;
-  std::vector<int32_t> row_pos;   // [total_q]
+  std::vector<int32_t> row_pos;   // [total_q] absolute position of each packed row
   std::vector<WorkItem> work;     // launch order (blockIdx.x)
   std::vector<MergeItem> merge;
+  std::vector<AppendItem> append; // one per (segment, cache block) slice
   int64_t num_tiles = 0;          // tiles x kv heads before splitting
   int64_t max_splits = 1;
   int64_t num_slots = 0;          // workspace partial slots

@@ -229,6 +229,22 @@ def test_forward_rejects_host_only_plan_and_null_plan(msa):
         msa.msa_forward(null, 16, 16, 16, 16, 16, stream=0)
 
 
+def test_kv_append_rejects_bad_arguments(msa):
+    inst = workloads.make_config(1)
+    plan = host_plan(msa, inst)
+    for bad in [(0, 64), (8 * 64, 0), (-64, 64), (260, 64), (256, 12)]:
+        with pytest.raises(msa.MsaError) as e:
+            msa.msa_kv_append(plan, 16, 16, 16, 16, 16, k_new_strides=bad, stream=0)
+        assert e.value.status == msa.MSA_ERR_INVALID_ARG
+        assert "strides" in msa.msa_last_error()
+    with pytest.raises(msa.MsaError) as e:
+        msa.msa_kv_append(plan, 16, 16, 16, 16, 16, stream=0)
+    assert e.value.status == msa.MSA_ERR_INVALID_ARG
+    assert "HOST_ONLY" in msa.msa_last_error()
+    with pytest.raises(msa.MsaError):
+        msa.msa_kv_append(msa.Plan(None, None), 16, 16, 16, 16, 16, stream=0)
+
+
 def _bad(inst, what):
     kv = inst.seq_kv_len.copy()
     ip = inst.seg_indptr.copy()

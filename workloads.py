@@ -96,6 +96,37 @@ def _bf16_normal(rng: np.random.Generator, shape) -> np.ndarray:
     return f32_to_bf16_bits(rng.standard_normal(size=shape, dtype=np.float32))
 
 
+def layout_cache(block_table: np.ndarray, num_blocks: int, k_logical, v_logical,
+                 block_size: int = BLOCK_SIZE) -> Tuple[np.ndarray, np.ndarray]:
+    """Place per-sequence logical K/V ([L_b, Hkv, d] bf16 bits) into zeroed
+    paged caches K [num_blocks, Hkv, bs, d] and V [num_blocks, Hkv, d, bs]
+    through ``block_table`` (whole blocks at a time: reshape + transpose)."""
+    B = len(k_logical)
+    Hkv, d = (k_logical[0].shape[1], k_logical[0].shape[2]) if B else (1, 1)
+    k_cache = np.zeros((num_blocks, Hkv, block_size, d), dtype=np.uint16)
+    v_cache = np.zeros((num_blocks, Hkv, d, block_size), dtype=np.uint16)
+    for b in range(B):
+        L = int(k_logical[b].shape[0])
+        nb = -(-L // block_size)
+        pad = nb * block_size - L
+        kb = np.concatenate([k_logical[b], np.zeros((pad, Hkv, d), np.uint16)])
+        vb = np.concatenate([v_logical[b], np.zeros((pad, Hkv, d), np.uint16)])
+        kb = kb.reshape(nb, block_size, Hkv, d)
+        vb = vb.reshape(nb, block_size, Hkv, d)
+        phys = block_table[b, :nb]
+        k_cache[phys] = kb.transpose(0, 2, 1, 3)
+        v_cache[phys] = vb.transpose(0, 2, 3, 1)
+    return k_cache, v_cache
+
+
+def make_fresh_kv(inst: Instance, seed: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Seeded fresh keys and values of every packed row: bf16 bits
+    [total_q, Hkv, d] each, drawn N(0, 1) like the rest of the inputs."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shape = (inst.total_q, inst.num_kv_heads, inst.head_dim)
+    return _bf16_normal(rng, shape), _bf16_normal(rng, shape)
+
+
 def build_instance(name: str, rng: np.random.Generator, kv_lens: Sequence[int],
                    segments: Sequence[Sequence[Tuple[int, int]]], num_q_heads: int,
                    num_kv_heads: int, head_dim: int, block_size: int = BLOCK_SIZE,
@@ -136,21 +167,9 @@ def build_instance(name: str, rng: np.random.Generator, kv_lens: Sequence[int],
     # K and V are drawn per sequence in logical (position) order, then placed
     # into their physical blocks; positions past L_b inside the last block
     # are zero.
-    k_cache = np.zeros((num_blocks, num_kv_heads, block_size, head_dim), dtype=np.uint16)
-    v_cache = np.zeros((num_blocks, num_kv_heads, head_dim, block_size), dtype=np.uint16)
     k_log = [_bf16_normal(rng, (int(L), num_kv_heads, head_dim)) for L in kv_lens]
     v_log = [_bf16_normal(rng, (int(L), num_kv_heads, head_dim)) for L in kv_lens]
-    for b in range(B):
-        L = int(kv_lens[b])
-        nb = blocks_per_seq[b]
-        pad = nb * block_size - L
-        kb = np.concatenate([k_log[b], np.zeros((pad, num_kv_heads, head_dim), np.uint16)])
-        vb = np.concatenate([v_log[b], np.zeros((pad, num_kv_heads, head_dim), np.uint16)])
-        kb = kb.reshape(nb, block_size, num_kv_heads, head_dim)
-        vb = vb.reshape(nb, block_size, num_kv_heads, head_dim)
-        phys = block_table[b, :nb]
-        k_cache[phys] = kb.transpose(0, 2, 1, 3)
-        v_cache[phys] = vb.transpose(0, 2, 3, 1)
+    k_cache, v_cache = layout_cache(block_table, num_blocks, k_log, v_log, block_size)
     return Instance(
         name=name, num_seqs=B, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
         head_dim=head_dim, block_size=block_size, scale=float(1.0 / np.sqrt(head_dim)),
