@@ -25,6 +25,9 @@
  *     V (channel-major inside a block):
  *        v_cache[blk*vsb + g*vsh + c*vsd + (j%bs)]
  *
+ *   The cache write before the attention (msa_oracle_kv_append): every packed
+ *   row's fresh key and value go to the slot of its absolute position.
+ *
  * Precision: inputs are bf16 bit patterns, widened exactly; every product,
  * sum, exponential and division is done in IEEE double, in the order the
  * definition is written (keys ascending, channels ascending).
