@@ -187,6 +187,102 @@ def report_all(path: str, steps: int, warmup: int):
             torch.cuda.empty_cache()
 
 
+ABLATION_CONTEXTS = (1024, 10240)
+ABLATION_BATCHES = (1, 8)
+
+
+def fused_ablation(path: str, steps: int, warmup: int):
+    """The paper's fused-kernel ablation (Sec. 6.3, Fig. ablation-fused) at the
+    attention level, Llama-3.1-8B head shape: requests of 1K and 10K tokens
+    ending with 128 new tokens, with a growing cached run placed as a prefix
+    (one segment), or as a suffix right before the new tokens computed with
+    one launch per segment (each launch covers that segment of every request)
+    or with one fused MSA launch.  One JSON line per (context, batch, cached)."""
+    import numpy as np
+    import torch
+    import workloads
+    import paper_2606_02964_amd as msa
+
+    Hq, Hkv, d = 32, 8, 128
+    stream = torch.cuda.current_stream()
+
+    def plan_for(shape, B, L, segs_per_seq):
+        ip = np.zeros(B + 1, np.int32)
+        ss, sl = [], []
+        for b in range(B):
+            for (st, n) in segs_per_seq:
+                ss.append(st)
+                sl.append(n)
+            ip[b + 1] = len(ss)
+        t0 = time.perf_counter()
+        plan = msa.msa_plan(shape, [L] * B, ip, ss, sl, stream=stream)
+        torch.cuda.synchronize()
+        return plan, (time.perf_counter() - t0) * 1e6
+
+    with open(path, "w") as out:
+        for L in ABLATION_CONTEXTS:
+            for B in ABLATION_BATCHES:
+                # one cache and one query buffer per (context, batch): every layout
+                # reads a prefix of the query rows and the same K/V
+                inst = workloads.make_layout(7000 + L + B, [L] * B, [[(0, L)]] * B, Hq, Hkv, d,
+                                             keep_logical=False)
+                dev = lambda bits: torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+                q, k, v = dev(inst.q), dev(inst.k_cache), dev(inst.v_cache)
+                bt = torch.from_numpy(np.ascontiguousarray(inst.block_table)).cuda()
+                o = torch.empty_like(q)
+                shape = msa.make_shape(B, Hq, Hkv, d, inst.max_blocks_per_seq, inst.num_blocks,
+                                       inst.scale)
+                step = (L - 128) // 7 // 16 * 16
+                for cached in [i * step for i in range(7)] + [L - 128]:
+                    rec = {"ctx": L, "batch": B, "cached": cached, "new_tokens": 128}
+                    for layout in ("prefix", "suffix"):
+                        segs = workloads.fused_ablation_layout(L, cached, layout)
+                        plan, plan_us = plan_for(shape, B, L, segs)
+                        info = plan.info()
+                        ws = (torch.empty(info["workspace_bytes"], dtype=torch.uint8, device="cuda")
+                              if info["workspace_bytes"] else None)
+                        ms = time_calls(lambda: msa.msa_forward(plan, q, k, v, bt, o, None, ws,
+                                                                stream=stream), stream, warmup, steps)
+                        key = "prefix" if layout == "prefix" else "suffix_msa"
+                        rec[key + "_us"] = round(ms * 1e3, 2)
+                        rec[key + "_plan_us"] = round(plan_us, 1)
+                        rec[key + "_rows"] = info["total_q"]
+                        rec[key + "_tflops"] = round(info["useful_flops"] / (ms * 1e-3) / 1e12, 1)
+                        if layout == "suffix":
+                            # one launch per segment: plan k holds segment k of every request,
+                            # its query rows are the packed rows of that segment
+                            plans, plan_us2, views = [], 0.0, []
+                            row = 0
+                            for (st, n) in segs:
+                                pk, pu = plan_for(shape, B, L, [(st, n)])
+                                plans.append(pk)
+                                plan_us2 += pu
+                            # packed rows of the fused layout are per request (seg0, seg1);
+                            # per-segment launches read their own contiguous query blocks
+                            wss = []
+                            for pk in plans:
+                                nb = pk.info()["workspace_bytes"]
+                                wss.append(torch.empty(nb, dtype=torch.uint8, device="cuda") if nb else None)
+                                views.append((q[row:row + pk.info()["total_q"]],
+                                              o[row:row + pk.info()["total_q"]]))
+                                row += pk.info()["total_q"]
+
+                            def per_segment():
+                                for pk, (qq, oo), w in zip(plans, views, wss):
+                                    msa.msa_forward(pk, qq, k, v, bt, oo, None, w, stream=stream)
+                            ms2 = time_calls(per_segment, stream, warmup, steps)
+                            rec["suffix_per_segment_us"] = round(ms2 * 1e3, 2)
+                            rec["suffix_per_segment_launches"] = len(plans)
+                            rec["suffix_per_segment_plan_us"] = round(plan_us2, 1)
+                            del plans, wss, views
+                        del plan, ws
+                    out.write(json.dumps(rec) + "\n")
+                    out.flush()
+                    log(f"fused ablation: {rec}")
+                del q, k, v, bt, o
+                torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -201,6 +297,8 @@ def main():
     ap.add_argument("--kv-split-tokens", type=int, default=0)
     ap.add_argument("--report", metavar="PATH", default=None,
                     help="only time every named workload and write one JSON line per case to PATH")
+    ap.add_argument("--fused-ablation", metavar="PATH", default=None,
+                    help="only run the single- vs per-segment-launch comparison; JSON lines to PATH")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES bytes (HBM counter calibration)")
     args = ap.parse_args()
@@ -220,6 +318,9 @@ def main():
         return
     if args.report:
         report_all(args.report, args.steps, args.warmup)
+        return
+    if args.fused_ablation:
+        fused_ablation(args.fused_ablation, args.steps, args.warmup)
         return
 
     import workloads

@@ -372,3 +372,24 @@ def test_plan_interpreter_matches_oracle(msa, oracle_lib, case, split):
     o, l = oracle_lib.forward(inst)
     np.testing.assert_allclose(io, o, rtol=0, atol=1e-12)
     np.testing.assert_allclose(il, l, rtol=0, atol=1e-12)
+
+
+def test_fused_ablation_layouts():
+    """Prefix and suffix placements of the same cached run compute the same
+    number of tokens; the suffix layout's segments are valid and end with the
+    128 new tokens (Sec. 6.3)."""
+    for ctx in (1024, 10240):
+        step = (ctx - 128) // 7 // 16 * 16
+        for cached in [i * step for i in range(7)] + [ctx - 128]:
+            pre = workloads.fused_ablation_layout(ctx, cached, "prefix")
+            suf = workloads.fused_ablation_layout(ctx, cached, "suffix")
+            assert sum(n for _, n in pre) == sum(n for _, n in suf) == ctx - cached
+            assert pre == [(cached, ctx - cached)]
+            assert suf[-1] == (ctx - 128, 128)
+            end = 0
+            for (s, n) in suf:
+                assert s >= end and n >= 1
+                end = s + n
+            assert end == ctx
+            if cached < ctx - 128:
+                assert suf[0] == (0, ctx - 128 - cached)

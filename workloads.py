@@ -286,6 +286,27 @@ CONFIG_DESCRIPTIONS = {
 }
 
 
+def fused_ablation_layout(ctx: int, cached: int, layout: str, new_tokens: int = 128):
+    """Query segments of one request in the paper's fused-kernel ablation
+    (Sec. 6.3): a context of ``ctx`` tokens that ends with ``new_tokens``
+    uncached tokens, of which ``cached`` earlier tokens are in the cache.
+
+    * ``"prefix"``: the cached tokens are the prefix [0, cached); one segment
+      [cached, ctx) is computed.
+    * ``"suffix"``: the cached tokens sit right before the new ones,
+      [ctx - new - cached, ctx - new); the evicted head [0, ctx - new - cached)
+      and the new tokens [ctx - new, ctx) are computed: two segments (one when
+      nothing before the cached run is evicted).
+    """
+    assert 0 <= cached <= ctx - new_tokens
+    if layout == "prefix":
+        return [(cached, ctx - cached)]
+    if layout == "suffix":
+        head = ctx - new_tokens - cached
+        return ([(0, head)] if head > 0 else []) + [(ctx - new_tokens, new_tokens)]
+    raise ValueError(layout)
+
+
 def make_config(cfg: int, seed: Optional[int] = None, keep_logical: bool = False,
                 decode_only: bool = False, **layout_kw) -> Instance:
     """Instance of named workload ``cfg`` (1..5).  Default seed = cfg.
