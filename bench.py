@@ -283,6 +283,80 @@ def fused_ablation(path: str, steps: int, warmup: int):
                 torch.cuda.empty_cache()
 
 
+def cost_model_fit(path: str, steps: int, warmup: int, n_points: int = 160, n_delta: int = 40):
+    """Fit the two-segment cost model of Sec. 4.3 (Eq. 4 and Eq. 6) to MSA
+    timings over a seeded (l1, q1, l2, q2) grid, Llama-3.1-8B head shape,
+    8 requests per launch; then check the eviction cost of Eq. 5 / Eq. 7 by
+    moving 256 tokens from l2 to q1 on a subset.  JSON lines to `path`: one
+    per sample, then one fit summary."""
+    import numpy as np
+    import torch
+    import workloads
+    import paper_2606_02964_amd as msa
+    from paper_2606_02964_amd import cost_model as cm
+
+    B, Hq, Hkv, d, max_ctx = 8, 32, 8, 128, 16384
+    stream = torch.cuda.current_stream()
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4303)
+    mb = max_ctx // 16
+    k = torch.randn((B * mb, Hkv, 16, d), generator=g, device="cuda").to(torch.bfloat16)
+    v = torch.randn((B * mb, Hkv, d, 16), generator=g, device="cuda").to(torch.bfloat16)
+    q = torch.randn((B * max_ctx, Hq, d), generator=g, device="cuda").to(torch.bfloat16)
+    o = torch.empty_like(q)
+    perm = np.random.Generator(np.random.PCG64(4303)).permutation(B * mb).astype(np.int32)
+    bt = torch.from_numpy(perm.reshape(B, mb)).cuda()
+    shape = msa.make_shape(B, Hq, Hkv, d, mb, B * mb, 1.0 / np.sqrt(d))
+
+    def measure(l1, q1, l2, q2):
+        segs = workloads.two_segment_layout(l1, q1, l2, q2)
+        ctx = l1 + q1 + l2 + q2
+        ip = np.arange(0, B * len(segs) + 1, len(segs), dtype=np.int32)
+        ss = [st for _ in range(B) for (st, _) in segs]
+        sl = [n for _ in range(B) for (_, n) in segs]
+        plan = msa.msa_plan(shape, [ctx] * B, ip, ss, sl, stream=stream)
+        info = plan.info()
+        ws = (torch.empty(info["workspace_bytes"], dtype=torch.uint8, device="cuda")
+              if info["workspace_bytes"] else None)
+        ms = time_calls(lambda: msa.msa_forward(plan, q, k, v, bt, o, None, ws, stream=stream),
+                        stream, warmup, steps)
+        return ms * 1e3, info
+
+    grid = workloads.cost_model_grid(4303, n_points)
+    samples = []
+    with open(path, "w") as out:
+        for (l1, q1, l2, q2) in grid:
+            us, info = measure(l1, q1, l2, q2)
+            samples.append((l1, q1, l2, q2, us))
+            out.write(json.dumps({"l1": l1, "q1": q1, "l2": l2, "q2": q2, "us": round(us, 2),
+                                  "useful_tflops": round(info["useful_flops"] / us / 1e6, 1)}) + "\n")
+            out.flush()
+        log(f"cost model: {len(samples)} samples timed")
+        fits = {m: cm.fit(m, samples) for m in cm.MODELS}
+        # eviction cost check: move 256 tokens (16 blocks) from l2 to q1
+        moves = [(l1, q1, l2, q2, us) for (l1, q1, l2, q2, us) in samples if l2 >= 256][:n_delta]
+        checks = []
+        for (l1, q1, l2, q2, us) in moves:
+            us2, _ = measure(l1, q1 + 256, l2 - 256, q2)
+            rec = {"l1": l1, "q1": q1, "l2": l2, "q2": q2, "dT_measured_us": round(us2 - us, 2)}
+            for m, (kc, _) in fits.items():
+                rec[f"dT_{m}_us"] = round(float(cm.delta_t_block(m, kc, l1, q1, l2, q2, bs=256)), 2)
+            checks.append(rec)
+            out.write(json.dumps({"delta_check": rec}) + "\n")
+        summary = {"fit": {}}
+        for m, (kc, r2) in fits.items():
+            meas = np.array([c["dT_measured_us"] for c in checks])
+            pred = np.array([c[f"dT_{m}_us"] for c in checks])
+            corr = float(np.corrcoef(meas, pred)[0, 1]) if len(checks) > 2 else None
+            summary["fit"][m] = {"coefficients_us": kc, "r2": r2, "dT_corr": corr,
+                                 "dT_median_abs_err_us": float(np.median(np.abs(meas - pred)))
+                                 if len(checks) else None}
+        summary["samples"] = len(samples)
+        summary["delta_checks"] = len(checks)
+        out.write(json.dumps({"summary": summary}) + "\n")
+        log(f"cost model fit: {json.dumps(summary)}")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -299,6 +373,8 @@ def main():
                     help="only time every named workload and write one JSON line per case to PATH")
     ap.add_argument("--fused-ablation", metavar="PATH", default=None,
                     help="only run the single- vs per-segment-launch comparison; JSON lines to PATH")
+    ap.add_argument("--cost-model", metavar="PATH", default=None,
+                    help="only time the cost-model grid (Sec. 4.3) and fit Eq. 4 / Eq. 6; JSON lines to PATH")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES bytes (HBM counter calibration)")
     args = ap.parse_args()
@@ -318,6 +394,9 @@ def main():
         return
     if args.report:
         report_all(args.report, args.steps, args.warmup)
+        return
+    if args.cost_model:
+        cost_model_fit(args.cost_model, args.steps, args.warmup)
         return
     if args.fused_ablation:
         fused_ablation(args.fused_ablation, args.steps, args.warmup)

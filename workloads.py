@@ -307,6 +307,30 @@ def fused_ablation_layout(ctx: int, cached: int, layout: str, new_tokens: int = 
     raise ValueError(layout)
 
 
+def cost_model_grid(seed: int, n: int, contexts=(2048, 4096, 8192, 12288, 16384),
+                    new_tokens=(64, 128, 256, 512, 1024)):
+    """Seeded two-segment layouts (l1, q1, l2, q2) for fitting the cost model
+    of Sec. 4.3: context [l1 cached][q1 computed][l2 cached][q2 computed]; the
+    context length and q2 are drawn from the given sets, the rest is cut at
+    two uniform block boundaries."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    pts = []
+    for _ in range(n):
+        N = int(rng.choice(contexts))
+        q2 = int(rng.choice(new_tokens))
+        rest_blocks = (N - q2) // BLOCK_SIZE
+        a, b = sorted(int(x) for x in rng.integers(0, rest_blocks + 1, 2))
+        l1, q1 = a * BLOCK_SIZE, (b - a) * BLOCK_SIZE
+        l2 = N - q2 - l1 - q1
+        pts.append((l1, q1, l2, q2))
+    return pts
+
+
+def two_segment_layout(l1: int, q1: int, l2: int, q2: int):
+    """Query segments of the cost model's layout (the q1 segment only if non-empty)."""
+    return ([(l1, q1)] if q1 > 0 else []) + [(l1 + q1 + l2, q2)]
+
+
 def make_config(cfg: int, seed: Optional[int] = None, keep_logical: bool = False,
                 decode_only: bool = False, **layout_kw) -> Instance:
     """Instance of named workload ``cfg`` (1..5).  Default seed = cfg.
