@@ -357,6 +357,53 @@ def cost_model_fit(path: str, steps: int, warmup: int, n_points: int = 160, n_de
         log(f"cost model fit: {json.dumps(summary)}")
 
 
+def evictor_bench(path: str):
+    """Control-plane cost of the block evictor (Sec. 4.5): a multi-turn serving
+    trace on an 8192-block cache (300 conversations x 8 turns = 2400
+    requests) is recorded once.  It is then replayed through the library's
+    two-tree evictor and through its O(n) scan, which must evict the same
+    blocks.  The oracle replays it too, for parity (its time is reported as
+    the plain-definition baseline).  Host-only; one JSON line to `path`."""
+    import numpy as np
+    import oracle
+    import workloads
+    import paper_2606_02964_amd as msa
+
+    params = dict(alpha=276.0, beta=276.0 / 40, tau0=276.0 * (1 - 1 / 40))
+    t0 = time.perf_counter()
+    trace = workloads.simulate_block_cache(msa.Evictor(**params), seed=2024, capacity=8192,
+                                           conversations=300, turns=8, lifespan_every=50)
+    sim_s = time.perf_counter() - t0
+    ev = trace.op == 2
+    rec = {"requests": trace.requests, "capacity_blocks": trace.capacity,
+           "ops": int(trace.op.size), "adds": int((trace.op == 0).sum()),
+           "removes": int((trace.op == 1).sum()), "evictions": int(ev.sum()),
+           "lifespan_updates": int((trace.op == 3).sum()),
+           "block_hit_rate": round(trace.hits / max(1, trace.hits + trace.misses), 4),
+           "simulation_s": round(sim_s, 2)}
+    for name, linear in (("tree", False), ("linear", True)):
+        e = msa.Evictor(**params, linear=linear)
+        t0 = time.perf_counter()
+        out = e.replay(trace.op, trace.ids, trace.t, trace.cost)
+        dt = time.perf_counter() - t0
+        assert np.array_equal(out[ev], trace.evicted[ev]), name
+        rec[f"{name}_s"] = round(dt, 4)
+        rec[f"{name}_us_per_op"] = round(dt / trace.op.size * 1e6, 4)
+        rec[f"{name}_us_per_eviction"] = round(dt / max(1, ev.sum()) * 1e6, 3)
+        rec[f"{name}_ms_per_request"] = round(dt / trace.requests * 1e3, 4)
+    t0 = time.perf_counter()
+    ref = oracle.evictor_replay(params["alpha"], params["beta"], params["tau0"], 1.0,
+                                trace.op, trace.ids, trace.t, trace.cost)
+    rec["oracle_s"] = round(time.perf_counter() - t0, 3)
+    rec["oracle_agrees"] = bool(np.array_equal(ref[ev], trace.evicted[ev]))
+    rec["linear_over_tree"] = round(rec["linear_s"] / rec["tree_s"], 1)
+    with open(path, "w") as out:
+        out.write(json.dumps(rec) + "\n")
+    log(f"evictor: {rec}")
+    if not rec["oracle_agrees"]:
+        raise SystemExit("evictor disagrees with the oracle")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -375,6 +422,8 @@ def main():
                     help="only run the single- vs per-segment-launch comparison; JSON lines to PATH")
     ap.add_argument("--cost-model", metavar="PATH", default=None,
                     help="only time the cost-model grid (Sec. 4.3) and fit Eq. 4 / Eq. 6; JSON lines to PATH")
+    ap.add_argument("--evictor", metavar="PATH", default=None,
+                    help="only time the block evictor on a recorded serving trace (host only)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES bytes (HBM counter calibration)")
     args = ap.parse_args()
@@ -383,6 +432,10 @@ def main():
         print("bench.py: this build runs on exactly one GPU; --gpus must be 1 "
               "(multi-GPU sharding is described in DESIGN.md, not implemented)", file=sys.stderr)
         sys.exit(2)
+
+    if args.evictor:
+        evictor_bench(args.evictor)
+        return
 
     import numpy as np
     import torch

@@ -5,6 +5,8 @@ leg may import this package.  The product (``paper_2606_02964_amd``) never
 does, and this package never imports the product.
 
 ``kv_append`` is the paged cache write of the rows' fresh K/V (Sec. 4.1, 5.3).
+``evictor_replay`` is the block-eviction policy (Sec. 4.2, Eq. 3, Eq. 9,
+Alg. 1's lambda, Eq. 10) evaluated by scanning every block at each eviction.
 ``forward`` is exact MSA (Sec. 2.1 Eq. 1 + Sec. 4.1 Eq. 2, causal by absolute
 position, GQA grouping h -> h / (Hq/Hkv)), computed in IEEE double by the
 plain C routine in ``msa_oracle.c``.
@@ -20,6 +22,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "msa_oracle.c")
+_SRC_EVICTOR = os.path.join(_HERE, "evictor_oracle.c")
 _LIB = os.path.join(_HERE, "libmsa_oracle.so")
 _lib = None
 
@@ -29,7 +32,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
-                               "-fno-fast-math", "-pthread", _SRC, "-o", tmp, "-lm"])
+                               "-fno-fast-math", "-pthread", _SRC, _SRC_EVICTOR, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -72,6 +75,9 @@ def _declare(lib):
         P, i64, i64, i64,                        # k cache (written)
         P, i64, i64, i64,                        # v cache (written)
         P]                                       # block table
+    if hasattr(lib, "msa_oracle_evictor_replay"):  # absent from single-file test builds
+        lib.msa_oracle_evictor_replay.restype = i64
+        lib.msa_oracle_evictor_replay.argtypes = [f64, f64, f64, f64, i64, P, P, P, P, P]
     lib.msa_oracle_total_rows.restype = i64
     lib.msa_oracle_total_rows.argtypes = [i32, P, P]
 
@@ -164,3 +170,24 @@ def kv_append(inst, k_new: np.ndarray, v_new: np.ndarray, lib=None) -> Tuple[np.
     if rc != 0:
         raise ValueError(f"msa_oracle_kv_append rejected its inputs (code {rc})")
     return k, v
+
+
+def evictor_replay(alpha: float, beta: float, tau0: float, lam: float, op, ids, t, cost,
+                   lib=None) -> np.ndarray:
+    """Replay evictor operations (codes 0 add, 1 remove, 2 evict, 3 lifespan);
+    returns the evicted id per op (-1 for non-evict ops).  Raises ValueError
+    naming the first operation the definition cannot apply."""
+    lib = _load() if lib is None else lib
+    c = np.ascontiguousarray
+    op = c(op, dtype=np.int32)
+    ids = c(ids, dtype=np.int64)
+    t = c(t, dtype=np.float64)
+    cost = c(cost, dtype=np.float64)
+    n = op.shape[0]
+    assert ids.shape == t.shape == cost.shape == (n,)
+    out = np.empty(n, dtype=np.int64)
+    rc = lib.msa_oracle_evictor_replay(float(alpha), float(beta), float(tau0), float(lam), n,
+                                       _ptr(op), _ptr(ids), _ptr(t), _ptr(cost), _ptr(out))
+    if rc != 0:
+        raise ValueError(f"msa_oracle_evictor_replay: operation {rc - 1} cannot be applied")
+    return out

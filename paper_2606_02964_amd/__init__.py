@@ -77,8 +77,35 @@ _lib.msa_last_error.argtypes = []
 _lib.msa_plan_export.restype = _i32
 _lib.msa_plan_export.argtypes = [_P, _P, _P, _P]
 
+_lib.msa_evictor_create.restype = _i32
+_lib.msa_evictor_create.argtypes = [_P, ctypes.POINTER(_P)]
+_lib.msa_evictor_destroy.restype = None
+_lib.msa_evictor_destroy.argtypes = [_P]
+_lib.msa_evictor_add.restype = _i32
+_lib.msa_evictor_add.argtypes = [_P, _i64, _f64, _f64]
+_lib.msa_evictor_remove.restype = _i32
+_lib.msa_evictor_remove.argtypes = [_P, _i64]
+_lib.msa_evictor_evict.restype = _i32
+_lib.msa_evictor_evict.argtypes = [_P, _f64, ctypes.POINTER(_i64)]
+_lib.msa_evictor_set_lambda.restype = _i32
+_lib.msa_evictor_set_lambda.argtypes = [_P, _f64]
+_lib.msa_evictor_set_lifespan.restype = _i32
+_lib.msa_evictor_set_lifespan.argtypes = [_P, _f64, ctypes.POINTER(_f64)]
+_lib.msa_evictor_size.restype = _i64
+_lib.msa_evictor_size.argtypes = [_P]
+_lib.msa_evictor_log_weight.restype = _i32
+_lib.msa_evictor_log_weight.argtypes = [_P, _i64, _f64, ctypes.POINTER(_f64)]
+_lib.msa_evictor_replay.restype = _i32
+_lib.msa_evictor_replay.argtypes = [_P, _i64, _P, _P, _P, _P, _P, ctypes.POINTER(_i64)]
+
 EXPORTED = ("msa_plan", "msa_plan_info", "msa_forward", "msa_kv_append", "msa_plan_destroy",
-            "msa_last_error", "msa_plan_export")
+            "msa_last_error", "msa_plan_export",
+            "msa_evictor_create", "msa_evictor_destroy", "msa_evictor_add", "msa_evictor_remove",
+            "msa_evictor_evict", "msa_evictor_set_lambda", "msa_evictor_set_lifespan",
+            "msa_evictor_size", "msa_evictor_log_weight", "msa_evictor_replay")
+
+MSA_EVICTOR_LINEAR = 1
+EVICTOR_OP_ADD, EVICTOR_OP_REMOVE, EVICTOR_OP_EVICT, EVICTOR_OP_LIFESPAN = 0, 1, 2, 3
 
 
 class MsaError(RuntimeError):
@@ -228,3 +255,73 @@ def make_shape(num_seqs: int, num_q_heads: int, num_kv_heads: int, head_dim: int
     return msa_shape(num_seqs, num_q_heads, num_kv_heads, head_dim, block_size,
                      max_blocks_per_seq, num_blocks, scale, qs[0], qs[1], os_[0], os_[1],
                      ks[0], ks[1], ks[2], vs[0], vs[1], vs[2])
+
+
+class msa_evictor_params(ctypes.Structure):
+    _fields_ = [("alpha", _f64), ("beta", _f64), ("tau0", _f64), ("lambda_", _f64),
+                ("flags", _i32), ("reserved", _i32 * 3)]
+
+
+class Evictor:
+    """Owning wrapper of an ``msa_evictor_t`` (include/msa_evictor.h): the
+    computation-aware block evictor (Sec. 4.2, Alg. 1)."""
+
+    def __init__(self, alpha: float, beta: float, tau0: float, lam: float = 1.0,
+                 linear: bool = False):
+        params = msa_evictor_params(alpha, beta, tau0, lam, MSA_EVICTOR_LINEAR if linear else 0)
+        h = _P()
+        _check(_lib.msa_evictor_create(ctypes.byref(params), ctypes.byref(h)))
+        self.handle = h.value
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _lib.msa_evictor_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def add(self, block_id: int, t_last: float, cost: float) -> None:
+        _check(_lib.msa_evictor_add(self.handle, int(block_id), float(t_last), float(cost)))
+
+    def remove(self, block_id: int) -> None:
+        _check(_lib.msa_evictor_remove(self.handle, int(block_id)))
+
+    def evict(self, t_now: float) -> int:
+        out = _i64()
+        _check(_lib.msa_evictor_evict(self.handle, float(t_now), ctypes.byref(out)))
+        return out.value
+
+    def set_lambda(self, lam: float) -> None:
+        _check(_lib.msa_evictor_set_lambda(self.handle, float(lam)))
+
+    def set_lifespan(self, tau: float) -> float:
+        out = _f64()
+        _check(_lib.msa_evictor_set_lifespan(self.handle, float(tau), ctypes.byref(out)))
+        return out.value
+
+    def __len__(self) -> int:
+        return int(_lib.msa_evictor_size(self.handle))
+
+    def log_weight(self, block_id: int, t: float) -> float:
+        out = _f64()
+        _check(_lib.msa_evictor_log_weight(self.handle, int(block_id), float(t), ctypes.byref(out)))
+        return out.value
+
+    def replay(self, op, ids, t, cost) -> np.ndarray:
+        """Apply a trace (codes EVICTOR_OP_*); returns the evicted id per op (-1 otherwise)."""
+        c = np.ascontiguousarray
+        op, ids = c(op, dtype=np.int32), c(ids, dtype=np.int64)
+        t, cost = c(t, dtype=np.float64), c(cost, dtype=np.float64)
+        n = op.shape[0]
+        out = np.empty(n, dtype=np.int64)
+        failed = _i64()
+        st = _lib.msa_evictor_replay(self.handle, n, op.ctypes.data, ids.ctypes.data,
+                                     t.ctypes.data, cost.ctypes.data, out.ctypes.data,
+                                     ctypes.byref(failed))
+        if st != MSA_OK:
+            raise MsaError(st, f"op {failed.value}: {msa_last_error()}")
+        return out

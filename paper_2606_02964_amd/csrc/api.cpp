@@ -9,6 +9,7 @@
 
 #include "msa.h"
 #include "append.h"
+#include "errors.h"
 #include "msa_internal.h"
 #include "plan.h"
 
@@ -38,6 +39,8 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 }  // namespace
+
+void msa::set_last_error(const std::string& msg) { g_last_error = msg; }
 
 extern "C" {
 

@@ -22,7 +22,7 @@ import pytest
 import workloads
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "msa.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("msa.h", "msa_evictor.h")]
 
 
 @pytest.fixture(scope="module")
@@ -32,9 +32,11 @@ def msa():
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(msa_[a-z_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(msa_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function(msa):
@@ -43,7 +45,7 @@ def test_library_exports_every_declared_function(msa):
             "msa_last_error", "msa_plan_export"} <= set(names)
     lib = ctypes.CDLL(msa.LIB_PATH)
     for n in names:
-        assert hasattr(lib, n), f"{n} declared in msa.h but not exported"
+        assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     nm = subprocess.run(["nm", "-D", "--defined-only", msa.LIB_PATH], capture_output=True,
                         text=True, check=True).stdout
     exported = set(re.findall(r"\bT (msa_\w+)", nm))

@@ -331,6 +331,116 @@ def two_segment_layout(l1: int, q1: int, l2: int, q2: int):
     return ([(l1, q1)] if q1 > 0 else []) + [(l1 + q1 + l2, q2)]
 
 
+# ---------------------------------------------------------------------------
+# block-cache traces for the evictor (Sec. 4.2, 4.5)
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class EvictorTrace:
+    """Operations recorded from a block-cache simulation (codes 0 add,
+    1 remove, 2 evict, 3 lifespan), with the evicted ids the driving evictor
+    returned and the cache statistics of the run."""
+    op: np.ndarray
+    ids: np.ndarray
+    t: np.ndarray
+    cost: np.ndarray
+    evicted: np.ndarray
+    requests: int
+    hits: int
+    misses: int
+    capacity: int
+
+
+def block_cost(index, tok_cost: float = 1.0, pair_cost: float = 1.0 / 4096,
+               block_size: int = BLOCK_SIZE):
+    """Synthetic recomputation cost of logical block ``index`` of a request:
+    a per-token part plus attention over every earlier key, summed over the
+    block's tokens (the position-linear form of Sec. 4.3).  By default
+    attention costs as much as the rest of the layer at 4K context."""
+    index = np.asarray(index, dtype=np.float64)
+    first = index * block_size
+    pairs = block_size * (first + 1) + block_size * (block_size - 1) / 2.0
+    return tok_cost * block_size + pair_cost * pairs
+
+
+def simulate_block_cache(evictor, seed: int, capacity: int = 8192, conversations: int = 300,
+                         turns: int = 8, first_prompt=(1024, 8192), turn_tokens=(200, 2048),
+                         max_tokens: int = 32768, think_time: float = 60.0,
+                         span: float = 3600.0, tokens_per_s: float = 20000.0,
+                         lifespan_every: int = 0) -> EvictorTrace:
+    """Multi-turn serving on a cache of ``capacity`` blocks, one request at a
+    time in arrival order.  Each conversation's context grows turn by turn;
+    the blocks of a request are held while it runs and handed to the evictor
+    (``add``) when it finishes.  A request takes its cached blocks back
+    (``remove``, a hit) and gets a fresh block for every missing one,
+    evicting (``evict``) when no free block is left.  Conversations start
+    uniformly over ``span`` seconds; turns follow after exponential think
+    times; a request runs ``tokens / tokens_per_s`` seconds.  With
+    ``lifespan_every`` = k > 0, every k-th request reports the mean observed
+    reuse gap as the lifespan (Sec. 5.1, Eq. 10)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    bs = BLOCK_SIZE
+    arrivals = []
+    for c in range(conversations):
+        t = float(rng.uniform(0.0, span))
+        ctx = int(rng.integers(first_prompt[0], first_prompt[1] + 1))
+        for k in range(turns):
+            arrivals.append((t, c, min(ctx, max_tokens)))
+            t += float(rng.exponential(think_time))
+            ctx += int(rng.integers(turn_tokens[0], turn_tokens[1] + 1))
+    arrivals.sort()
+    ops, ids, ts, costs, ev_out = [], [], [], [], []
+    cached = set()
+    released = {}
+    free = capacity
+    clock = 0.0
+    hits = misses = 0
+    gaps = []
+
+    def record(o, i, t, c, e=-1):
+        ops.append(o)
+        ids.append(i)
+        ts.append(t)
+        costs.append(c)
+        ev_out.append(e)
+
+    for n_req, (t_arr, c, ctx) in enumerate(arrivals):
+        clock = max(clock, t_arr)
+        n = -(-ctx // bs)
+        assert n <= capacity, "a request larger than the cache"
+        blocks = [c * (max_tokens // bs + 1) + i for i in range(n)]
+        want = []
+        for b in blocks:
+            if b in cached:
+                evictor.remove(b)
+                record(1, b, 0.0, 0.0)
+                gaps.append(clock - released[b])
+                hits += 1
+            else:
+                want.append(b)
+        misses += len(want)
+        while free < len(want):
+            victim = evictor.evict(clock)
+            record(2, -1, clock, 0.0, victim)
+            cached.discard(victim)
+            free += 1
+        free -= len(want)
+        cached.update(want)
+        clock += ctx / tokens_per_s
+        for i, b in enumerate(blocks):
+            cost = float(block_cost(i))
+            evictor.add(b, clock, cost)
+            record(0, b, clock, cost)
+            released[b] = clock
+        if lifespan_every and (n_req + 1) % lifespan_every == 0 and gaps:
+            tau = float(np.mean(gaps[-4096:]))
+            evictor.set_lifespan(tau)
+            record(3, -1, tau, 0.0)
+    return EvictorTrace(np.asarray(ops, np.int32), np.asarray(ids, np.int64),
+                        np.asarray(ts, np.float64), np.asarray(costs, np.float64),
+                        np.asarray(ev_out, np.int64), len(arrivals), hits, misses, capacity)
+
+
 def make_config(cfg: int, seed: Optional[int] = None, keep_logical: bool = False,
                 decode_only: bool = False, **layout_kw) -> Instance:
     """Instance of named workload ``cfg`` (1..5).  Default seed = cfg.
