@@ -77,7 +77,7 @@ typedef struct msa_plan_s *msa_plan_t;
 typedef struct msa_shape {
   int32_t num_seqs;           /* B >= 0 */
   int32_t num_q_heads;        /* Hq >= 1 */
-  int32_t num_kv_heads;       /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv <= 128 */
+  int32_t num_kv_heads;       /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv <= 256 */
   int32_t head_dim;           /* d: 64 or 128 */
   int32_t block_size;         /* bs: 16 */
   int32_t max_blocks_per_seq; /* row stride of block_table (entries) */
@@ -91,7 +91,7 @@ typedef struct msa_shape {
 
 /* Planner options; a zero field means "choose automatically". */
 typedef struct msa_plan_opts {
-  int32_t q_tile_tokens;   /* cap on query tokens per tile (<= 128 / (Hq/Hkv)) */
+  int32_t q_tile_tokens;   /* cap on query tokens per tile (<= tile rows / (Hq/Hkv)) */
   int32_t kv_split_tokens; /* force key splits of this many keys (multiple of 64) */
   int32_t flags;           /* MSA_PLAN_* bits */
   int32_t reserved[5];     /* must be zero */
@@ -102,6 +102,13 @@ typedef struct msa_plan_opts {
 #define MSA_PLAN_HOST_ONLY 1
 /* Disable the cost-based automatic key splitting (forced splits still apply). */
 #define MSA_PLAN_NO_AUTO_SPLIT 2
+/* Force the tile width (query rows x heads per workgroup).  Without either
+ * flag the planner takes 256-row tiles (one workgroup per CU; each K/V step
+ * is loaded once for twice the rows) when the plan has many tiles, and
+ * 128-row tiles (two workgroups per CU, more concurrent key streams) for
+ * small and decode-heavy plans.  The two flags are exclusive. */
+#define MSA_PLAN_TILE_ROWS_128 4
+#define MSA_PLAN_TILE_ROWS_256 8
 
 /* Figures describing a plan. */
 typedef struct msa_plan_info_t {
@@ -115,6 +122,7 @@ typedef struct msa_plan_info_t {
   double tile_flops;        /* flops the tiles issue (waves holding rows), incl. masked waste */
   double planned_bytes;     /* Q + O + K/V bytes the executed tiles request */
   double min_bytes;         /* Q + O + K/V of visible keys once per (seq, kv head) */
+  int64_t tile_rows;        /* rows per tile of this plan: 128 or 256 */
 } msa_plan_info_t;
 
 /*
@@ -136,8 +144,9 @@ typedef struct msa_plan_info_t {
  *   out         receives the plan; destroy with msa_plan_destroy
  *
  * Returns MSA_ERR_INVALID_ARG for malformed descriptors or shapes,
- * MSA_ERR_UNSUPPORTED for head_dim not in {64, 128}, block_size != 16 or
- * Hq / Hkv > 128, MSA_ERR_OUT_OF_MEMORY, MSA_ERR_DEVICE.
+ * MSA_ERR_UNSUPPORTED for head_dim not in {64, 128}, block_size != 16,
+ * Hq / Hkv > 256, or Hq / Hkv > 128 with MSA_PLAN_TILE_ROWS_128;
+ * MSA_ERR_OUT_OF_MEMORY; MSA_ERR_DEVICE.
  */
 msa_status msa_plan(const msa_shape *shape, const int32_t *seq_kv_len, const int32_t *seg_indptr,
                     const int32_t *seg_start, const int32_t *seg_len, const msa_plan_opts *opts,

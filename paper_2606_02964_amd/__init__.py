@@ -24,6 +24,13 @@ LIB_PATH = os.path.join(_HERE, "libmsa.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_02964_amd.build`")
+# Device buffers and streams come from PyTorch: load it first so that the
+# library binds to the HIP runtime torch already holds (a second runtime in
+# the process would see other streams, and possibly no device).
+try:
+    import torch  # noqa: F401
+except ImportError:  # plain C users: the system HIP runtime
+    pass
 _lib = ctypes.CDLL(LIB_PATH)
 
 MSA_OK = 0
@@ -33,6 +40,8 @@ MSA_ERR_OUT_OF_MEMORY = 3
 MSA_ERR_DEVICE = 4
 MSA_PLAN_HOST_ONLY = 1
 MSA_PLAN_NO_AUTO_SPLIT = 2
+MSA_PLAN_TILE_ROWS_128 = 4
+MSA_PLAN_TILE_ROWS_256 = 8
 
 _i32, _i64, _f32, _f64, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 
@@ -55,7 +64,8 @@ class msa_plan_opts(ctypes.Structure):
 class msa_plan_info_t(ctypes.Structure):
     _fields_ = [("total_q", _i64), ("num_work", _i64), ("num_tiles", _i64), ("num_merge", _i64),
                 ("max_splits", _i64), ("workspace_bytes", _i64), ("useful_flops", _f64),
-                ("tile_flops", _f64), ("planned_bytes", _f64), ("min_bytes", _f64)]
+                ("tile_flops", _f64), ("planned_bytes", _f64), ("min_bytes", _f64),
+                ("tile_rows", _i64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -86,9 +86,10 @@ msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int
     if (n_work) std::memcpy(plan->staging.data() + off_work, hp.work.data(), n_work);
     if (n_merge) std::memcpy(plan->staging.data() + off_merge, hp.merge.data(), n_merge);
     if (n_append) std::memcpy(plan->staging.data() + off_append, hp.append.data(), n_append);
-    if (hipGetDevice(&plan->device) != hipSuccess) {
+    const hipError_t gd = hipGetDevice(&plan->device);
+    if (gd != hipSuccess) {
       delete plan;
-      return set_error(MSA_ERR_DEVICE, "msa_plan: hipGetDevice failed");
+      return set_error(MSA_ERR_DEVICE, std::string("msa_plan: hipGetDevice failed: ") + hipGetErrorString(gd));
     }
     void* dev = nullptr;
     if (hipMalloc(&dev, bytes) != hipSuccess) {
@@ -126,6 +127,7 @@ msa_status msa_plan_info(msa_plan_t plan, msa_plan_info_t* info) {
   info->tile_flops = hp.tile_flops;
   info->planned_bytes = hp.planned_bytes;
   info->min_bytes = hp.min_bytes;
+  info->tile_rows = hp.tile_rows;
   return MSA_OK;
 }
 
@@ -196,7 +198,7 @@ msa_status msa_forward(msa_plan_t plan, const void* q, const void* k_cache, cons
   p.group = hp.group;
   p.tile_tokens = hp.tile_tokens;
   p.scale_log2 = s.scale * 1.4426950408889634f;
-  int rc = msa::launch_attn(p, s.head_dim, (int)hp.work.size(), hip_stream);
+  int rc = msa::launch_attn(p, s.head_dim, hp.tile_rows, (int)hp.work.size(), hip_stream);
   if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string("msa_forward: attention launch failed: ") +
                                                     hipGetErrorString((hipError_t)rc));
   if (!hp.merge.empty()) {
@@ -209,6 +211,7 @@ msa_status msa_forward(msa_plan_t plan, const void* q, const void* k_cache, cons
     m.o_sh = s.o_stride_head;
     m.num_q_heads = s.num_q_heads;
     m.group = hp.group;
+    m.tile_rows = hp.tile_rows;
     rc = msa::launch_merge(m, s.head_dim, (int)hp.merge.size(), hip_stream);
     if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string("msa_forward: merge launch failed: ") +
                                                       hipGetErrorString((hipError_t)rc));

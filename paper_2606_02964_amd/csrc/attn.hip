@@ -1,8 +1,10 @@
 // attn.hip -- gfx950 kernels of Multi-Segment Attention.
 //
-// msa_attn: one workgroup (4 waves, 256 threads) per work item = up to 128
-// query rows of one sequence sharing one KV head, over one key range.  Per
-// 64-key step:
+// msa_attn: one workgroup per work item = up to 32 rows per wave (4 or 8
+// waves: 128 or 256 rows) of one sequence sharing one KV head, over one key
+// range.  The wide form loads each K/V step once for twice the rows (one
+// workgroup per CU); the narrow form keeps two workgroups per CU for small
+// plans.  Per 64-key step:
 //   - paged gather: the 4 cache blocks of the step are looked up in the block
 //     table and copied to LDS with 16-byte loads (K as [key][d], V as [d][key]
 //     since the V cache is channel-major inside a block), double buffered;
@@ -50,7 +52,6 @@ struct Tile {
   static constexpr int kBytesK = kKvStep * kPitchK;
   static constexpr int kBytesV = D * kPitchV;
   static constexpr int kStage = kBytesK + kBytesV;
-  static constexpr int kRounds = kKvStep * D / 8 / 256;  // 16-byte chunks per thread, per tensor
 };
 
 __device__ __forceinline__ int swap_bits23(int m) {
@@ -78,9 +79,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 // weights stay <= 2^8
 constexpr float kRescaleLog2 = 8.0f;
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
+template <int D, int W>
+__global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   using T = Tile<D>;
+  constexpr int kThreads = 64 * W;
+  constexpr int kRows = 32 * W;                          // tile rows
+  constexpr int kRounds = kKvStep * D / 8 / kThreads;    // 16-byte chunks per thread, per tensor
   __shared__ __attribute__((aligned(16))) char smem[2 * T::kStage];
 
   const WorkItem w = p.work[blockIdx.x];
@@ -120,12 +124,12 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
   }
 
   // Gather geometry.  One cache block of one KV head is 16 keys x D
-  // channels = 2*D chunks of 16 bytes per tensor; 256 threads cover
-  // 256 / (2*D) blocks per round, kRounds rounds cover the 4 blocks of a
-  // step.  Thread tid takes chunk cb = tid % (2*D) of block
-  // i * (256 / (2*D)) + tid / (2*D) in round i.
+  // channels = 2*D chunks of 16 bytes per tensor; the workgroup's threads
+  // cover kThreads / (2*D) blocks per round, kRounds rounds cover the 4
+  // blocks of a step.  Thread tid takes chunk cb = tid % (2*D) of block
+  // i * (kThreads / (2*D)) + tid / (2*D) in round i.
   constexpr int kChunksPerBlock = 2 * D;
-  constexpr int kBlocksPerRound = 256 / kChunksPerBlock;
+  constexpr int kBlocksPerRound = kThreads / kChunksPerBlock;
   const int cb = tid % kChunksPerBlock;
   const int bsub = tid / kChunksPerBlock;  // wave-uniform
   const int kkey = cb / (D / 8), kdch = cb % (D / 8);
@@ -136,15 +140,15 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
   const char* kbase = reinterpret_cast<const char*>(p.k + (int64_t)w.kv_head * p.k_sh);
   const char* vbase = reinterpret_cast<const char*>(p.v + (int64_t)w.kv_head * p.v_sh);
   const int32_t* bt = p.block_table + (int64_t)w.seq * p.max_blocks;
-  int klds[T::kRounds], vlds[T::kRounds];
+  int klds[kRounds], vlds[kRounds];
 #pragma unroll
-  for (int i = 0; i < T::kRounds; ++i) {
+  for (int i = 0; i < kRounds; ++i) {
     const int blk = i * kBlocksPerRound + bsub;
     klds[i] = (blk * 16 + kkey) * T::kPitchK + kdch * 16;
     vlds[i] = T::kBytesK + vch * T::kPitchV + (blk * 16 + vhalf * 8) * 2;
   }
 
-  uint4 kr[T::kRounds], vr[T::kRounds];
+  uint4 kr[kRounds], vr[kRounds];
   // global -> registers for the step starting at key kb; blocks at or past
   // kv_hi are not read (their block-table entries need not be valid)
   auto load = [&](int kb) {
@@ -152,7 +156,7 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) ids[j] = kb + j * kBlockSize < w.kv_hi ? bt[(kb >> 4) + j] : -1;
 #pragma unroll
-    for (int i = 0; i < T::kRounds; ++i) {
+    for (int i = 0; i < kRounds; ++i) {
       const int id = kBlocksPerRound == 1 ? ids[i] : ids[i * kBlocksPerRound + bsub];
       if (id >= 0) {
         kr[i] = *reinterpret_cast<const uint4*>(kbase + id * ksb + koff);
@@ -165,7 +169,7 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
   };
   auto store = [&](char* st) {
 #pragma unroll
-    for (int i = 0; i < T::kRounds; ++i) {
+    for (int i = 0; i < kRounds; ++i) {
       *reinterpret_cast<uint4*>(st + klds[i]) = kr[i];
       *reinterpret_cast<uint4*>(st + vlds[i]) = vr[i];
     }
@@ -294,7 +298,7 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
     if (p.lse && hl == 0)
       p.lse[(int64_t)tok * p.num_q_heads + head] = (m_ref + __log2f(l_tot)) * kLn2;
   } else {
-    float* slot = p.ws + (int64_t)w.out_slot * kTileRows * (D + 1);
+    float* slot = p.ws + (int64_t)w.out_slot * kRows * (D + 1);
     const bool empty = !(l_tot > 0.0f);  // no visible key in this split
     const float inv = empty ? 0.0f : 1.0f / l_tot;
     float* orow = slot + r * D;
@@ -308,7 +312,7 @@ __global__ __launch_bounds__(256, 2) void msa_attn_kernel(AttnParams p) {
         *reinterpret_cast<f32x4*>(orow + dt * 32 + g4 * 8 + hl * 4) = v;
       }
     if (hl == 0)
-      slot[kTileRows * D + r] = empty ? -__builtin_inff() : (m_ref + __log2f(l_tot)) * kLn2;
+      slot[kRows * D + r] = empty ? -__builtin_inff() : (m_ref + __log2f(l_tot)) * kLn2;
   }
 }
 
@@ -320,19 +324,20 @@ __global__ __launch_bounds__(256) void msa_merge_kernel(MergeParams p) {
   const int G = p.group;
   const int rows = mi.nrows * G;
   const int sub = threadIdx.x % kThreadsPerRow;
-  const int64_t slot_f = (int64_t)kTileRows * (D + 1);
+  const int R = p.tile_rows;
+  const int64_t slot_f = (int64_t)R * (D + 1);
   for (int r = threadIdx.x / kThreadsPerRow; r < rows; r += kRowsPerPass) {
     const int t = r / G, hh = r - t * G;
     const int tok = mi.row0 + t, head = mi.kv_head * G + hh;
     float mx = -__builtin_inff();
     for (int s = 0; s < mi.nsplit; ++s)
-      mx = fmaxf(mx, p.ws[(int64_t)(mi.slot0 + s) * slot_f + kTileRows * D + r]);
+      mx = fmaxf(mx, p.ws[(int64_t)(mi.slot0 + s) * slot_f + (int64_t)R * D + r]);
     const float mu = mx == -__builtin_inff() ? 0.0f : mx;
     float L = 0.0f;
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int s = 0; s < mi.nsplit; ++s) {
       const float* base = p.ws + (int64_t)(mi.slot0 + s) * slot_f;
-      const float wgt = __builtin_amdgcn_exp2f((base[kTileRows * D + r] - mu) * kLog2e);
+      const float wgt = __builtin_amdgcn_exp2f((base[(int64_t)R * D + r] - mu) * kLog2e);
       L += wgt;
       const f32x4 os = *reinterpret_cast<const f32x4*>(base + r * D + sub * 4);
       acc += wgt * os;
@@ -348,13 +353,17 @@ __global__ __launch_bounds__(256) void msa_merge_kernel(MergeParams p) {
 
 }  // namespace
 
-int launch_attn(const AttnParams& p, int head_dim, int num_work, void* stream) {
+int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_work, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (num_work <= 0) return 0;
-  if (head_dim == 128)
-    hipLaunchKernelGGL(msa_attn_kernel<128>, dim3(num_work), dim3(256), 0, s, p);
-  else if (head_dim == 64)
-    hipLaunchKernelGGL(msa_attn_kernel<64>, dim3(num_work), dim3(256), 0, s, p);
+  if (head_dim == 128 && tile_rows == kTileRowsNarrow)
+    hipLaunchKernelGGL((msa_attn_kernel<128, 4>), dim3(num_work), dim3(256), 0, s, p);
+  else if (head_dim == 128 && tile_rows == kTileRowsWide)
+    hipLaunchKernelGGL((msa_attn_kernel<128, 8>), dim3(num_work), dim3(512), 0, s, p);
+  else if (head_dim == 64 && tile_rows == kTileRowsNarrow)
+    hipLaunchKernelGGL((msa_attn_kernel<64, 4>), dim3(num_work), dim3(256), 0, s, p);
+  else if (head_dim == 64 && tile_rows == kTileRowsWide)
+    hipLaunchKernelGGL((msa_attn_kernel<64, 8>), dim3(num_work), dim3(512), 0, s, p);
   else
     return (int)hipErrorInvalidValue;
   return (int)hipGetLastError();

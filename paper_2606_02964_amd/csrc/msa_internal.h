@@ -1,6 +1,6 @@
 // msa_internal.h -- tables shared by the host planner and the gfx950 kernels.
 //
-// A work item is one workgroup: up to kTileRows query rows of one sequence
+// A work item is one workgroup: up to tile_rows query rows of one sequence
 // that share one KV head (tokens x the G = Hq/Hkv query heads of the group,
 // row r <-> token r / G, head r % G) and one contiguous key range.  The
 // planner packs consecutive query tokens of a sequence into a tile even
@@ -13,8 +13,12 @@
 
 namespace msa {
 
-constexpr int kTileRows = 128;   // rows per workgroup: 4 waves x 32 rows
-constexpr int kWaves = 4;
+// Two tile widths: 128 rows (4 waves x 32 rows, two workgroups per CU) for
+// small or decode-heavy plans, 256 rows (8 waves, one workgroup per CU) for
+// plans with many tiles: a wider tile loads each K/V step once for twice the
+// rows.
+constexpr int kTileRowsNarrow = 128;
+constexpr int kTileRowsWide = 256;
 constexpr int kKvStep = 64;      // keys per main-loop iteration (4 blocks of 16)
 constexpr int kBlockSize = 16;
 
@@ -41,9 +45,9 @@ struct MergeItem {
 };
 static_assert(sizeof(MergeItem) == 32, "MergeItem is exported as 8 int32");
 
-// Workspace slot of one partial tile result: O [kTileRows][d] fp32 (already
-// divided by its own softmax sum), then lse [kTileRows] fp32 (natural log).
-inline int64_t slot_floats(int head_dim) { return (int64_t)kTileRows * (head_dim + 1); }
+// Workspace slot of one partial tile result: O [tile_rows][d] fp32 (already
+// divided by its own softmax sum), then lse [tile_rows] fp32 (natural log).
+inline int64_t slot_floats(int head_dim, int tile_rows) { return (int64_t)tile_rows * (head_dim + 1); }
 
 // Arguments of the attention kernel.
 struct AttnParams {
@@ -74,10 +78,11 @@ struct MergeParams {
   int64_t o_st, o_sh;
   int32_t num_q_heads;
   int32_t group;
+  int32_t tile_rows;  // rows of a workspace slot
 };
 
 // Launchers (attn.hip).  Return a hipError_t value as int.
-int launch_attn(const AttnParams& p, int head_dim, int num_work, void* stream);
+int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_work, void* stream);
 int launch_merge(const MergeParams& p, int head_dim, int num_merge, void* stream);
 
 }  // namespace msa

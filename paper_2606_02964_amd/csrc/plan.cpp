@@ -7,9 +7,13 @@
 //   1. rows: each packed query row gets its absolute position (its causal
 //      limit is position + 1 keys);
 //   2. tiles: consecutive rows of one sequence are packed into tiles of up to
-//      128 / G tokens (G = Hq / Hkv query heads share one KV head), across
-//      segment gaps as long as the keys masked for the earlier rows stay a
-//      small fraction of the tile's work;
+//      tile_rows / G tokens (G = Hq / Hkv query heads share one KV head),
+//      across segment gaps as long as the keys masked for the earlier rows
+//      stay a small fraction of the tile's work.  tile_rows is 256 (one
+//      workgroup per CU, each K/V step loaded once for 256 rows) when the
+//      plan has enough tiles to fill the GPU several times over, else 128
+//      (two workgroups per CU, more concurrent key streams for small and
+//      decode-heavy plans);
 //   3. units: tile x KV head, keys [0, max position in tile + 1);
 //   4. key splits: units much longer than the average share of a workgroup
 //      slot are cut into 64-aligned key ranges, merged later by log-sum-exp;
@@ -27,7 +31,8 @@ namespace msa {
 namespace {
 
 constexpr int kXcds = 8;
-constexpr int kSlots = 256 * 2;          // CUs x resident workgroups per CU
+constexpr int kCUs = 256;
+constexpr int64_t kWideMinTiles = 1024;  // narrow tiles from which wide tiles pay
 constexpr double kWasteFrac = 0.125;     // masked keys allowed per tile, relative
 constexpr int64_t kMinSplitKeys = 1024;  // never split below this many keys
 
@@ -53,8 +58,11 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   if (opts) o = *opts;
   for (int i = 0; i < 5; ++i)
     if (o.reserved[i] != 0) return fail(err, MSA_ERR_INVALID_ARG, "opts.reserved must be zero");
-  if (o.flags & ~(MSA_PLAN_HOST_ONLY | MSA_PLAN_NO_AUTO_SPLIT))
+  if (o.flags & ~(MSA_PLAN_HOST_ONLY | MSA_PLAN_NO_AUTO_SPLIT | MSA_PLAN_TILE_ROWS_128 |
+                  MSA_PLAN_TILE_ROWS_256))
     return fail(err, MSA_ERR_INVALID_ARG, "unknown opts.flags bits");
+  if ((o.flags & MSA_PLAN_TILE_ROWS_128) && (o.flags & MSA_PLAN_TILE_ROWS_256))
+    return fail(err, MSA_ERR_INVALID_ARG, "MSA_PLAN_TILE_ROWS_128 and _256 are exclusive");
 
   if (s.num_seqs < 0) return fail(err, MSA_ERR_INVALID_ARG, "num_seqs < 0");
   if (s.num_q_heads < 1 || s.num_kv_heads < 1)
@@ -62,7 +70,9 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   if (s.num_q_heads % s.num_kv_heads != 0)
     return fail(err, MSA_ERR_INVALID_ARG, "num_q_heads must be a multiple of num_kv_heads");
   const int32_t G = s.num_q_heads / s.num_kv_heads;
-  if (G > kTileRows) return fail(err, MSA_ERR_UNSUPPORTED, "num_q_heads / num_kv_heads > 128");
+  if (G > kTileRowsWide) return fail(err, MSA_ERR_UNSUPPORTED, "num_q_heads / num_kv_heads > 256");
+  if (G > kTileRowsNarrow && (o.flags & MSA_PLAN_TILE_ROWS_128))
+    return fail(err, MSA_ERR_UNSUPPORTED, "128-row tiles need num_q_heads / num_kv_heads <= 128");
   if (s.head_dim <= 0) return fail(err, MSA_ERR_INVALID_ARG, "head_dim <= 0");
   if (s.head_dim != 64 && s.head_dim != 128)
     return fail(err, MSA_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
@@ -77,10 +87,8 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
       !aligned8(s.k_stride_tok) || !aligned8(s.v_stride_block) || !aligned8(s.v_stride_head) ||
       !aligned8(s.v_stride_dim))
     return fail(err, MSA_ERR_INVALID_ARG, "strides must be positive multiples of 8 elements");
-  int32_t tile_tokens = kTileRows / G;
-  if (o.q_tile_tokens < 0 || o.q_tile_tokens > tile_tokens)
-    return fail(err, MSA_ERR_INVALID_ARG, "q_tile_tokens must be in [0, 128 / (Hq/Hkv)]");
-  if (o.q_tile_tokens > 0) tile_tokens = o.q_tile_tokens;
+  if (o.q_tile_tokens < 0 || o.q_tile_tokens > kTileRowsWide / G)
+    return fail(err, MSA_ERR_INVALID_ARG, "q_tile_tokens must be in [0, tile_rows / (Hq/Hkv)]");
   if (o.kv_split_tokens < 0 || o.kv_split_tokens % kKvStep != 0)
     return fail(err, MSA_ERR_INVALID_ARG, "kv_split_tokens must be a non-negative multiple of 64");
 
@@ -100,7 +108,6 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   P = HostPlan{};
   P.shape = s;
   P.group = G;
-  P.tile_tokens = tile_tokens;
   std::vector<int64_t> seq_row0(B + 1, 0);
   std::vector<int32_t> seq_maxpos(B, -1);
   int64_t total = 0;
@@ -136,6 +143,28 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
       for (int32_t k = seg_indptr[b]; k < seg_indptr[b + 1]; ++k)
         for (int32_t t = 0; t < seg_len[k]; ++t) P.row_pos[(size_t)r++] = seg_start[k] + t;
   }
+  // tile width: forced by a flag, else wide when the narrow tiling would
+  // give enough tiles (counted without the splits at segment gaps)
+  {
+    int32_t rows = kTileRowsNarrow;
+    if (o.flags & MSA_PLAN_TILE_ROWS_256) {
+      rows = kTileRowsWide;
+    } else if (!(o.flags & MSA_PLAN_TILE_ROWS_128)) {
+      const int64_t tok = kTileRowsNarrow / std::max<int32_t>(1, std::min<int32_t>(G, kTileRowsNarrow));
+      int64_t narrow = 0;
+      for (int32_t b = 0; b < B; ++b) narrow += (seq_row0[b + 1] - seq_row0[b] + tok - 1) / tok;
+      narrow *= s.num_kv_heads;
+      if (G > kTileRowsNarrow || narrow >= kWideMinTiles) rows = kTileRowsWide;
+    }
+    P.tile_rows = rows;
+    P.tile_tokens = rows / G;
+    if (o.q_tile_tokens > P.tile_tokens)
+      return fail(err, MSA_ERR_INVALID_ARG, "q_tile_tokens must be in [0, tile_rows / (Hq/Hkv)]");
+    if (o.q_tile_tokens > 0) P.tile_tokens = o.q_tile_tokens;
+  }
+  const int32_t tile_tokens = P.tile_tokens;
+  const int64_t slots_total = (int64_t)kCUs * (P.tile_rows == kTileRowsWide ? 1 : 2);
+
   // slices of the cache write: each segment cut at cache-block boundaries
   {
     int64_t r = 0;
@@ -188,7 +217,7 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     double total_steps = 0;
     for (const Unit& u : units) total_steps += (double)(steps(u.kv_hi) + 1);
     // aim at >= 2 work items per workgroup slot for the longest units
-    const int64_t share = (int64_t)std::ceil(total_steps / (2.0 * kSlots)) * kKvStep;
+    const int64_t share = (int64_t)std::ceil(total_steps / (2.0 * slots_total)) * kKvStep;
     split_keys = std::max<int64_t>(kMinSplitKeys, share);
   }
   struct Piece {
@@ -221,7 +250,7 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     P.max_splits = std::max<int64_t>(P.max_splits, nsplit);
   }
   P.num_slots = slots;
-  P.workspace_bytes = slots * slot_floats(d) * (int64_t)sizeof(float);
+  P.workspace_bytes = slots * slot_floats(d, P.tile_rows) * (int64_t)sizeof(float);
 
   // 5. order: groups (seq, kv head) -> XCD queues, longest first
   const int64_t ngroups = (int64_t)B * Hkv;

@@ -15,6 +15,7 @@ import ctypes
 import os
 import re
 import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -93,7 +94,7 @@ def check_plan(inst, row_pos, work, merge, info, G):
         if nrows == 0:
             continue
         assert 0 <= g < Hkv and 0 <= row0 and row0 + nrows <= total
-        assert nrows * G <= 128
+        assert nrows * G <= info["tile_rows"]
         assert (rseq[row0:row0 + nrows] == seq).all(), "tile crosses a sequence"
         assert lo % 64 == 0 and 0 <= lo < hi
         tile_max = int(row_pos[row0:row0 + nrows].max())
@@ -123,7 +124,8 @@ def check_plan(inst, row_pos, work, merge, info, G):
     assert (covered == 1).all(), "every (row, kv head) must be in exactly one tile"
     assert len(merged) == len(merge)
     assert info["total_q"] == total
-    assert info["workspace_bytes"] == len(slots_seen) * 128 * (inst.head_dim + 1) * 4
+    assert info["tile_rows"] in (128, 256)
+    assert info["workspace_bytes"] == len(slots_seen) * info["tile_rows"] * (inst.head_dim + 1) * 4
     useful = 4.0 * inst.head_dim * inst.num_q_heads * float((row_pos.astype(np.float64) + 1).sum())
     assert abs(info["useful_flops"] - useful) <= 1e-9 * max(1.0, useful)
 
@@ -138,9 +140,10 @@ PLAN_CASES = [
 
 @pytest.mark.parametrize("case", PLAN_CASES)
 @pytest.mark.parametrize("split", [0, 64, 192, 1024])
-def test_plan_structure(msa, case, split):
+@pytest.mark.parametrize("tile_flag", [0, 4, 8])  # auto, 128-row, 256-row tiles
+def test_plan_structure(msa, case, split, tile_flag):
     inst = workloads.make_random(keep_logical=False, **case)
-    plan = host_plan(msa, inst, kv_split_tokens=split)
+    plan = host_plan(msa, inst, kv_split_tokens=split, flags=tile_flag)
     info = plan.info()
     row_pos, work, merge = msa.msa_plan_export(plan)
     check_plan(inst, row_pos, work, merge, info, inst.num_q_heads // inst.num_kv_heads)
@@ -302,10 +305,20 @@ def test_plan_rejects_bad_options(msa):
         with pytest.raises(msa.MsaError) as e:
             host_plan(msa, inst, **kw)
         assert e.value.status == msa.MSA_ERR_INVALID_ARG
-    big_group = workloads.make_layout(10, [64], [[(0, 4)]], 256, 1, 64)
+    too_big_group = workloads.make_layout(10, [64], [[(0, 4)]], 512, 1, 64)
     with pytest.raises(msa.MsaError) as e:
-        host_plan(msa, big_group)
+        host_plan(msa, too_big_group)
     assert e.value.status == msa.MSA_ERR_UNSUPPORTED
+    big_group = workloads.make_layout(10, [64], [[(0, 4)]], 256, 1, 64)
+    assert host_plan(msa, big_group).info()["tile_rows"] == 256
+    with pytest.raises(msa.MsaError) as e:
+        host_plan(msa, big_group, flags=msa.MSA_PLAN_TILE_ROWS_128)
+    assert e.value.status == msa.MSA_ERR_UNSUPPORTED
+    with pytest.raises(msa.MsaError) as e:
+        host_plan(msa, inst, flags=msa.MSA_PLAN_TILE_ROWS_128 | msa.MSA_PLAN_TILE_ROWS_256)
+    assert e.value.status == msa.MSA_ERR_INVALID_ARG
+    # the token cap follows the tile width: 128 / 2 = 64 narrow, 128 wide
+    assert host_plan(msa, inst, q_tile_tokens=65, flags=msa.MSA_PLAN_TILE_ROWS_256).info()["tile_rows"] == 256
 
 
 # --------------------------------------------------------------------------
@@ -363,12 +376,13 @@ def interpret_plan(inst, row_pos, work, merge):
     return out_o, out_l
 
 
+@pytest.mark.parametrize("tile_flag", [4, 8])
 @pytest.mark.parametrize("split", [0, 64, 128])
 @pytest.mark.parametrize("case", PLAN_CASES[:2] + PLAN_CASES[3:])
-def test_plan_interpreter_matches_oracle(msa, oracle_lib, case, split):
+def test_plan_interpreter_matches_oracle(msa, oracle_lib, case, split, tile_flag):
     case = dict(case, max_len=min(case["max_len"], 400))
     inst = workloads.make_random(keep_logical=False, **case)
-    plan = host_plan(msa, inst, kv_split_tokens=split)
+    plan = host_plan(msa, inst, kv_split_tokens=split, flags=tile_flag)
     row_pos, work, merge = msa.msa_plan_export(plan)
     io, il = interpret_plan(inst, row_pos, work, merge)
     o, l = oracle_lib.forward(inst)
@@ -395,3 +409,26 @@ def test_fused_ablation_layouts():
             assert end == ctx
             if cached < ctx - 128:
                 assert suf[0] == (0, ctx - 128 - cached)
+
+
+def test_tile_width_choice(msa):
+    """Wide (256-row) tiles for plans with many tiles, narrow (128-row) tiles
+    for small and decode-only plans; flags force either."""
+    for cfg, rows in ((1, 128), (2, 256), (3, 256), (4, 256), (5, 256)):
+        assert host_plan(msa, make_layout_only(cfg)).info()["tile_rows"] == rows, cfg
+    decode = workloads.make_config(5, decode_only=True)
+    assert host_plan(msa, decode).info()["tile_rows"] == 128
+    assert host_plan(msa, decode, flags=msa.MSA_PLAN_TILE_ROWS_256).info()["tile_rows"] == 256
+    assert host_plan(msa, make_layout_only(2), flags=msa.MSA_PLAN_TILE_ROWS_128).info()["tile_rows"] == 128
+
+
+def test_one_hip_runtime_per_process():
+    """Importing the package before torch must not load a second HIP runtime
+    (torch's streams and device pointers belong to torch's runtime)."""
+    code = ("import paper_2606_02964_amd, torch\n"
+            "maps = open('/proc/self/maps').read().split('\\n')\n"
+            "paths = {l.split()[-1] for l in maps if 'libamdhip64' in l}\n"
+            "print(len(paths))\n")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                         check=True).stdout.strip()
+    assert out == "1", out

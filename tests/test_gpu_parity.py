@@ -58,27 +58,49 @@ RANDOM = [
 ]
 
 
+# plan flags: automatic tile width, forced 128-row tiles, forced 256-row tiles
+TILES = [0, msa.MSA_PLAN_TILE_ROWS_128, msa.MSA_PLAN_TILE_ROWS_256]
+
+
+@pytest.mark.parametrize("tile", TILES)
 @pytest.mark.parametrize("case", RANDOM)
 @pytest.mark.parametrize("split", [0, 64, 320])
-def test_random_full_parity(oracle_lib, case, split):
+def test_random_full_parity(oracle_lib, case, split, tile):
     seed, B, Hq, Hkv, d, max_len, max_segs = case
     inst = workloads.make_random(seed, num_seqs=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d,
                                  max_len=max_len, max_segs=max_segs, keep_logical=False)
-    _, _, plan = check_full(inst, oracle_lib, kv_split_tokens=split)
+    _, _, plan = check_full(inst, oracle_lib, kv_split_tokens=split, flags=tile)
     max_keys = max((s + n for b in range(inst.num_seqs) for (s, n) in inst.segments(b)), default=0)
     if split and max_keys > split:
         assert plan.info()["num_merge"] > 0
 
 
-def test_block_aligned_and_adjacent_segments(oracle_lib):
+@pytest.mark.parametrize("tile", TILES[1:])
+def test_block_aligned_and_adjacent_segments(oracle_lib, tile):
     inst = workloads.make_layout(31, [1024, 777], [[(0, 16), (16, 32), (64, 64), (512, 512)],
                                                   [(0, 1), (1, 1), (400, 377)]], 32, 8, 128)
-    check_full(inst, oracle_lib)
+    check_full(inst, oracle_lib, flags=tile)
 
 
-def test_prefill_and_decode_layouts(oracle_lib):
+@pytest.mark.parametrize("tile", TILES[1:])
+def test_prefill_and_decode_layouts(oracle_lib, tile):
     inst = workloads.make_layout(32, [1000, 513, 64], [[(0, 1000)], [(512, 1)], [(63, 1)]], 8, 2, 128)
-    check_full(inst, oracle_lib)
+    check_full(inst, oracle_lib, flags=tile)
+
+
+@pytest.mark.parametrize("case", [RANDOM[1], RANDOM[4], RANDOM[6]])
+def test_tile_width_is_bitwise_invariant(case):
+    """A row's arithmetic does not depend on which rows share its tile, so
+    without key splits the 128-row and 256-row kernels agree bit for bit."""
+    seed, B, Hq, Hkv, d, max_len, max_segs = case
+    inst = workloads.make_random(seed, num_seqs=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d,
+                                 max_len=max_len, max_segs=max_segs, keep_logical=False)
+    dinst = DeviceInstance(inst)
+    o1, l1, p1 = run(dinst, flags=msa.MSA_PLAN_NO_AUTO_SPLIT | msa.MSA_PLAN_TILE_ROWS_128)
+    o2, l2, p2 = run(dinst, flags=msa.MSA_PLAN_NO_AUTO_SPLIT | msa.MSA_PLAN_TILE_ROWS_256)
+    assert p1.info()["tile_rows"] == 128 and p2.info()["tile_rows"] == 256
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
 
 
 def test_sequences_sharing_physical_prefix_blocks(oracle_lib):
@@ -114,12 +136,15 @@ def _sample_items(inst, n, seed):
     return rows.astype(np.int64), heads.astype(np.int32)
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5, "5-decode"])
 def test_named_workload_sampled_parity(oracle_lib, cfg):
     """Full-size workloads in the benchmark's launch configuration (automatic
     plan): every output finite and inside the convex hull of V, sampled
     (row, head) items against the oracle."""
-    inst = workloads.make_config(cfg)
+    if cfg == "5-decode":
+        inst, cfg = workloads.make_config(5, decode_only=True), 6
+    else:
+        inst = workloads.make_config(cfg)
     d = DeviceInstance(inst)
     o, lse, plan = run(d)
     go = o.float()
