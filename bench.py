@@ -175,6 +175,7 @@ def report_all(path: str, steps: int, warmup: int):
                 "planned_bytes_gbs": round(info["planned_bytes"] / t / 1e9, 1),
                 "tile_flop_ratio": round(info["tile_flops"] / max(info["useful_flops"], 1.0), 4),
                 "work_items": info["num_work"], "split_tiles": info["num_merge"],
+                "tile_rows": info["tile_rows"],
                 "max_splits": info["max_splits"],
                 "append_us_per_call": round(ms_app * 1e3, 2),
                 "append_gbs": round(app_bytes / (ms_app * 1e-3) / 1e9, 1),
@@ -549,6 +550,7 @@ def main():
             "useful_tflop_per_call": round(useful / 1e12, 4),
             "kernels_per_call": 1 + (1 if info["num_merge"] else 0),
             "work_items": info["num_work"],
+            "tile_rows": info["tile_rows"],
         },
         "us_per_call": round(ms * 1e3, 1),
         "us_per_call_cold": round(cold_ms * 1e3, 1) if cold_ms else None,
