@@ -1,29 +1,34 @@
 // attn.hip -- gfx950 kernels of Multi-Segment Attention.
 //
-// msa_attn: one workgroup per work item = up to 32 rows per wave (4 or 8
-// waves: 128 or 256 rows) of one sequence sharing one KV head, over one key
-// range.  The wide form loads each K/V step once for twice the rows (one
-// workgroup per CU); the narrow form keeps two workgroups per CU for small
-// plans.  Per 64-key step:
-//   - paged gather: the 4 cache blocks of the step are looked up in the block
-//     table and copied to LDS with 16-byte loads (K as [key][d], V as [d][key]
-//     since the V cache is channel-major inside a block), double buffered;
-//   - S^T = K Q^T on v_mfma_f32_32x32x16_bf16.  K is the A operand, so in the
-//     result each lane holds one query row (column) and 16 of the 32 keys:
+// msa_attn: one workgroup of W waves (W = 4 or 8: 128 or 256 rows, 32 rows
+// per wave) per work item: query rows of one sequence sharing one KV head,
+// over one key range.  Each 64-key step:
+//   - paged gather: the step's 4 cache blocks are looked up in the block
+//     table and copied straight into LDS (global_load_lds, 16 bytes a lane,
+//     no staging registers): K as [key][d] rows, V as the cache's
+//     channel-major [d][16 keys] pages, 16-byte chunks XOR-swizzled so that
+//     every operand read is free of bank conflicts.  K runs one step ahead of
+//     V in rings of two stages;
+//   - S^T = K Q^T on v_mfma_f32_32x32x16_bf16.  K is the A operand, so each
+//     lane holds one query row (a column of S^T) and 16 of the 32 keys: the
 //     row max and row sum need one exchange with the lane 32 apart only;
 //   - per-row causal limit: key j is visible to the row at absolute position
-//     p iff j <= p (applied only on steps that reach past the smallest
-//     position of the wave);
+//     p iff j <= p (only on steps that reach past the wave's smallest
+//     position; a wave stops computing after the step holding its largest
+//     position, while it keeps copying its share and meeting the barriers);
 //   - online softmax in fp32 in the exp2 domain: the row max is taken on the
 //     raw scores, scale * log2(e) enters one FMA per score; the reference max
 //     only moves (and O is only rescaled) when a row's max grows by more than
-//     2^8, so most steps skip the rescale; the row sum adds the bf16-rounded
-//     weights with v_dot2 against (1, 1);
-//   - O^T += V^T P^T on the same MFMA: P is the B operand and is packed to
-//     bf16 straight from the score registers.  The A-operand row order of K is
-//     permuted (bits 2 and 3 of the row index swapped) so that the 8 scores a
-//     lane feeds to one PV step are 8 consecutive keys, matching a single
-//     16-byte LDS read of V^T.
+//     2^8; the row sum adds the bf16-rounded weights with v_dot2 against (1, 1);
+//   - O^T += V^T P^T on the same MFMA, P packed to bf16 straight from the
+//     score registers.  The A-operand row order of K is permuted (bits 2 and 3
+//     of the row index swapped) so that the 8 scores a lane feeds to one PV
+//     step are 8 consecutive keys, a single 16-byte LDS read of V^T.
+// Steps whose successor needs no mask run software-pipelined in pairs: the
+// QK MFMAs of step j+1 are interleaved with the exponentials of step j, and
+// the PV MFMAs of step j with the row max of step j+1, so that every MFMA is
+// followed by independent vector work.  The diagonal steps and the last one
+// run the same operations without overlap.
 // msa_merge: combines the per-split partials of a split tile by log-sum-exp.
 #include <hip/hip_runtime.h>
 
@@ -45,13 +50,19 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kLog2e = 1.4426950408889634f;
 
+// LDS layout of one stage (no padding; 16-byte chunks XOR-swizzled so that
+// every 16-lane group of an operand read hits 16 distinct bank groups):
+//   K tile: 64 keys x D channels, row = key (2*D bytes); chunk c of row k is
+//           stored at chunk c ^ ((k / rows per 256 bytes) mod chunks per row)
+//   V tile: page-major, 4 blocks x D channels x 16 keys (32 bytes per channel
+//           row); the two 16-byte halves of channel d swap when bit 3 of d is set
 template <int D>
 struct Tile {
-  static constexpr int kPitchK = D * 2 + 16;        // bytes per key row of the K tile
-  static constexpr int kPitchV = kKvStep * 2 + 16;  // bytes per channel row of the V^T tile
-  static constexpr int kBytesK = kKvStep * kPitchK;
-  static constexpr int kBytesV = D * kPitchV;
+  static constexpr int kBytesK = kKvStep * D * 2;
+  static constexpr int kBytesV = kKvStep * D * 2;
   static constexpr int kStage = kBytesK + kBytesV;
+  static constexpr int kPage = kBlockSize * D * 2;  // bytes of one block of K or V
+  static constexpr int kDmaPerPage = kPage / 1024;  // 1 KB per wave-wide 16-byte copy
 };
 
 __device__ __forceinline__ int swap_bits23(int m) {
@@ -74,6 +85,25 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// 16 bytes per lane from global memory straight into LDS at
+// lds + 16 * lane (a wave copies 1 KB); completion is tracked by vmcnt
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void_t*)lds, 16, 0, 0);
+}
+// wait until at most n copies issued by this wave are outstanding
+template <int n>
+__device__ __forceinline__ void wait_dma() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
+}
+// workgroup barrier that orders LDS accesses only: the compiler's
+// __syncthreads() would also drain every outstanding global->LDS copy
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // running-max threshold of the lazy rescale: the reference max only moves
 // when a row's max grows by more than this (log2 units), so the unnormalised
 // weights stay <= 2^8
@@ -82,16 +112,16 @@ constexpr float kRescaleLog2 = 8.0f;
 template <int D, int W>
 __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   using T = Tile<D>;
-  constexpr int kThreads = 64 * W;
-  constexpr int kRows = 32 * W;                          // tile rows
-  constexpr int kRounds = kKvStep * D / 8 / kThreads;    // 16-byte chunks per thread, per tensor
-  __shared__ __attribute__((aligned(16))) char smem[2 * T::kStage];
+  constexpr int kRows = 32 * W;  // tile rows
+  // K ring (2 steps) then V ring (2 steps); K runs one step ahead of V
+  __shared__ __attribute__((aligned(1024))) char smem[2 * T::kBytesK + 2 * T::kBytesV];
 
   const WorkItem w = p.work[blockIdx.x];
   if (w.nrows == 0) return;  // padding item (uniform over the workgroup)
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63, hl = lane >> 5, ln = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
   const int G = p.group;
   const int r = wave * 32 + ln;  // tile row
   const int t = r / G, hh = r - t * G;
@@ -100,13 +130,15 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   const int head = w.kv_head * G + hh;
   const int pos = valid ? p.row_pos[tok] : -1;
 
-  // wave-wide smallest and largest causal limit (wave-uniform branches)
+  // wave-wide smallest and largest causal limit
   int pmin = valid ? pos : INT_MAX, pmax = pos;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     pmin = min(pmin, __shfl_xor(pmin, off));
     pmax = max(pmax, __shfl_xor(pmax, off));
   }
+  pmin = __builtin_amdgcn_readfirstlane(pmin);
+  pmax = __builtin_amdgcn_readfirstlane(pmax);
 
   // Q fragments (B operand): row r, channels kk*16 + hl*8 .. +8
   bf16x8 qf[D / 16];
@@ -123,55 +155,75 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
     }
   }
 
-  // Gather geometry.  One cache block of one KV head is 16 keys x D
-  // channels = 2*D chunks of 16 bytes per tensor; the workgroup's threads
-  // cover kThreads / (2*D) blocks per round, kRounds rounds cover the 4
-  // blocks of a step.  Thread tid takes chunk cb = tid % (2*D) of block
-  // i * (kThreads / (2*D)) + tid / (2*D) in round i.
-  constexpr int kChunksPerBlock = 2 * D;
-  constexpr int kBlocksPerRound = kThreads / kChunksPerBlock;
-  const int cb = tid % kChunksPerBlock;
-  const int bsub = tid / kChunksPerBlock;  // wave-uniform
-  const int kkey = cb / (D / 8), kdch = cb % (D / 8);
-  const int vch = cb >> 1, vhalf = cb & 1;
-  const uint32_t koff = (uint32_t)(kkey * p.k_st + kdch * 8) * 2u;   // bytes inside a block
-  const uint32_t voff = (uint32_t)(vch * p.v_sd + vhalf * 8) * 2u;
-  const int64_t ksb = p.k_sb * 2, vsb = p.v_sb * 2;                   // bytes per block
+  // Gather geometry: a page (one block of K or V) is kDmaPerPage wave-wide
+  // 16-byte copies (see the layout note above); lane offsets inside a block:
+  constexpr int kChunksPerRow = 2 * D / 16;            // 16-byte chunks per K row
+  constexpr int kRowsPerCopy = 64 / kChunksPerRow;     // K rows per 1 KB copy
+  constexpr int kRowsPer256 = 256 / (2 * D);           // K rows sharing one 256-byte bank row
+  auto kswz = [](int k) { return (k / kRowsPer256) & (kChunksPerRow - 1); };
+  uint32_t kgo[T::kDmaPerPage];                       // byte offsets inside a cache block
+#pragma unroll
+  for (int q = 0; q < T::kDmaPerPage; ++q) {
+    const int kin = q * kRowsPerCopy + lane / kChunksPerRow;
+    const int lc = (lane % kChunksPerRow) ^ kswz(kin);
+    kgo[q] = (uint32_t)(kin * p.k_st + lc * 8) * 2u;
+  }
+  // V copy q moves channels q*32 .. q*32+31: the same lane pattern, shifted
+  // by 32 channels (bit 3 of the channel, hence the half swap, is unchanged)
+  const uint32_t vgo0 = (uint32_t)((lane >> 1) * p.v_sd + (((lane & 1) ^ ((lane >> 4) & 1)) * 8)) * 2u;
+  const uint32_t vgq = (uint32_t)(32 * p.v_sd) * 2u;
+  const int64_t ksb = p.k_sb * 2, vsb = p.v_sb * 2;  // bytes per block
   const char* kbase = reinterpret_cast<const char*>(p.k + (int64_t)w.kv_head * p.k_sh);
   const char* vbase = reinterpret_cast<const char*>(p.v + (int64_t)w.kv_head * p.v_sh);
   const int32_t* bt = p.block_table + (int64_t)w.seq * p.max_blocks;
-  int klds[kRounds], vlds[kRounds];
-#pragma unroll
-  for (int i = 0; i < kRounds; ++i) {
-    const int blk = i * kBlocksPerRound + bsub;
-    klds[i] = (blk * 16 + kkey) * T::kPitchK + kdch * 16;
-    vlds[i] = T::kBytesK + vch * T::kPitchV + (blk * 16 + vhalf * 8) * 2;
-  }
-
-  uint4 kr[kRounds], vr[kRounds];
-  // global -> registers for the step starting at key kb; blocks at or past
-  // kv_hi are not read (their block-table entries need not be valid)
-  auto load = [&](int kb) {
-    int ids[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) ids[j] = kb + j * kBlockSize < w.kv_hi ? bt[(kb >> 4) + j] : -1;
-#pragma unroll
-    for (int i = 0; i < kRounds; ++i) {
-      const int id = kBlocksPerRound == 1 ? ids[i] : ids[i * kBlocksPerRound + bsub];
-      if (id >= 0) {
-        kr[i] = *reinterpret_cast<const uint4*>(kbase + id * ksb + koff);
-        vr[i] = *reinterpret_cast<const uint4*>(vbase + id * vsb + voff);
-      } else {
-        kr[i] = make_uint4(0, 0, 0, 0);
-        vr[i] = make_uint4(0, 0, 0, 0);
-      }
-    }
+  auto kbuf = [&](int s) -> char* { return smem + __builtin_amdgcn_readfirstlane((s & 1) * T::kBytesK); };
+  auto vbuf = [&](int s) -> char* {
+    return smem + __builtin_amdgcn_readfirstlane(2 * T::kBytesK + (s & 1) * T::kBytesV);
   };
-  auto store = [&](char* st) {
+  const int n = (w.kv_hi - w.kv_lo + kKvStep - 1) / kKvStep;
+  // A step has 8 pages: the K and the V page of each of its 4 blocks (page
+  // pg: block pg & 3, V if pg >= 4); wave w copies pages w, w + W, ...
+  // issue(sk, sv) copies the K pages of step sk and the V pages of step sv
+  // (-1: none).  All block ids are read before the first copy, so no id load
+  // waits behind copies of the same call.  A block at or past kv_hi is not
+  // read; its V page is zero-filled instead (its K page keeps old values:
+  // those keys are masked by selection, so never meet arithmetic).
+  constexpr int kPagesPerWave = 8 / W;
+  auto issue = [&](int sk, int sv) {
+    int64_t ids[kPagesPerWave];
+    bool have[kPagesPerWave], zero[kPagesPerWave];
 #pragma unroll
-    for (int i = 0; i < kRounds; ++i) {
-      *reinterpret_cast<uint4*>(st + klds[i]) = kr[i];
-      *reinterpret_cast<uint4*>(st + vlds[i]) = vr[i];
+    for (int k = 0; k < kPagesPerWave; ++k) {
+      const int pg = wave + k * W;
+      const int bi = pg & 3;
+      const int st = pg >= 4 ? sv : sk;
+      const bool live = st >= 0 && st < n;
+      const int kb = w.kv_lo + st * kKvStep;
+      have[k] = live && kb + bi * kBlockSize < w.kv_hi;
+      zero[k] = live && !have[k] && pg >= 4;
+      ids[k] = have[k] ? (int64_t)__builtin_amdgcn_readfirstlane(bt[(kb >> 4) + bi]) : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kPagesPerWave; ++k) {
+      const int pg = wave + k * W;
+      const int bi = pg & 3;
+      if (have[k]) {
+        if (pg < 4) {
+          const char* kg = kbase + ids[k] * ksb;
+          char* kd = kbuf(sk) + bi * T::kPage;
+#pragma unroll
+          for (int q = 0; q < T::kDmaPerPage; ++q) dma16(kg + kgo[q], kd + q * 1024);
+        } else {
+          const char* vg = vbase + ids[k] * vsb;
+          char* vd = vbuf(sv) + bi * T::kPage;
+#pragma unroll
+          for (int q = 0; q < T::kDmaPerPage; ++q) dma16(vg + q * vgq + vgo0, vd + q * 1024);
+        }
+      } else if (zero[k]) {
+#pragma unroll
+        for (int q = 0; q < T::kDmaPerPage; ++q)
+          *reinterpret_cast<uint4*>(vbuf(sv) + bi * T::kPage + q * 1024 + lane * 16) = make_uint4(0, 0, 0, 0);
+      }
     }
   };
 
@@ -182,43 +234,59 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.0f;
-  const int klane = swap_bits23(ln) * T::kPitchK + hl * 16;
-  const int vlane = T::kBytesK + ln * T::kPitchV + hl * 16;
+  const int krow_m = swap_bits23(ln);                 // key row of MFMA row ln (tile kt adds 32)
+  const int vsw = (hl ^ ((ln >> 3) & 1)) * 16;        // V half swizzle of channel dt*32 + ln
+  constexpr int kQk = 2 * (D / 16);                   // QK MFMAs per step, ordered (kk, kt)
+  constexpr int kPv = 4 * (D / 32);                   // PV MFMAs per step, ordered (ks, dt)
+  constexpr int kElPerQk = 32 / kQk;                  // scores handled per QK MFMA
+  constexpr int kElPerPv = 32 / kPv;                  // scores handled per PV MFMA
 
-  // one 64-key step over the LDS stage `cur`
-  auto step = [&](const char* cur, int kb, auto masked) {
-    constexpr bool kMasked = decltype(masked)::value;
-    // S^T = K Q^T: two 32-key tiles
-    f32x16 s[2];
+  // K operand of QK MFMA i of step s (register i of a lane: key row kt*32 + krow_m)
+  auto kread = [&](int s, int i) -> bf16x8 {
+    const int kk = i >> 1, kt = i & 1;
+    const int row = kt * 32 + krow_m;
+    return *reinterpret_cast<const bf16x8*>(kbuf(s) + row * (2 * D) + (((kk * 2 + hl) ^ kswz(row)) * 16));
+  };
+  auto vread = [&](int s, int i) -> bf16x8 {
+    const int ks = i / (D / 32), dt = i % (D / 32);
+    return *reinterpret_cast<const bf16x8*>(vbuf(s) + ks * T::kPage + (dt * 32 + ln) * 32 + vsw);
+  };
+  // score e (0..31) of a lane sits in tile e/16, register e%16
+
+  f32x16 sbuf[2][2];
+  float mx_next = -__builtin_inff();
+
+  // QK of step s into sbuf[b] (no interleaving; prologue only)
+  auto qk_plain = [&](int b, int s) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      const char* krow = cur + kt * 32 * T::kPitchK + klane;
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + kk * 32);
-        if (kk == 0) {
-          const f32x16 zero = {};
-          s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0], zero, 0, 0, 0);
-        } else {
-          s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[kt], 0, 0, 0);
-        }
+    for (int i = 0; i < kQk; ++i) {
+      const bf16x8 a = kread(s, i);
+      const int kk = i >> 1, kt = i & 1;
+      if (kk == 0) {
+        const f32x16 zero = {};
+        sbuf[b][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0], zero, 0, 0, 0);
+      } else {
+        sbuf[b][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sbuf[b][kt], 0, 0, 0);
       }
     }
-    // lane (hl, ln), register i of tile kt holds key kb + kt*32 + (i/8)*16 + hl*8 + i%8
-    if constexpr (kMasked) {
-      const int lim = pos - kb - hl * 8;
+  };
+  // mask + max of step s held in sbuf[b] (plain, prologue only)
+  auto max_plain = [&](int b, int s, auto masked) {
+    constexpr bool kM = decltype(masked)::value;
+    const int lim = pos - (w.kv_lo + s * kKvStep) - hl * 8;
+    float mx = -__builtin_inff();
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          s[kt][i] = (kt * 32 + (i >> 3) * 16 + (i & 7)) <= lim ? s[kt][i] : -__builtin_inff();
+    for (int e = 0; e < 32; ++e) {
+      float x = sbuf[b][e >> 4][e & 15];
+      if constexpr (kM) x = ((e >> 4) * 32 + ((e & 15) >> 3) * 16 + (e & 7)) <= lim ? x : -__builtin_inff();
+      sbuf[b][e >> 4][e & 15] = x;
+      mx = fmaxf(mx, x);
     }
-    float mx = fmaxf(s[0][0], s[0][1]);
-#pragma unroll
-    for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[0][i]);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[1][i]);
-    const float m_blk = pair_max(mx) * c;
+    mx_next = mx;
+  };
+  // move the reference max of the step whose raw max is mx_next (rare)
+  auto rescale = [&]() {
+    const float m_blk = pair_max(mx_next) * c;
     const bool grow = m_blk > m_ref + kRescaleLog2;
     if (__any(grow)) {  // wave-uniform
       const float alpha = grow ? __builtin_amdgcn_exp2f(m_ref - m_blk) : 1.0f;
@@ -227,58 +295,152 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
     }
-    // a row with no visible key so far keeps m_ref = -inf; its scores are -inf too
-    const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
-    uint32_t pk[2][8];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int i = 0; i < 16; i += 2)
-        pk[kt][i >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][i], c, nm)),
-                                     __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][i + 1], c, nm)));
-    // the row sum adds the same bf16-rounded weights that enter the PV
-    // product, so the normalised weights sum to one exactly
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-    float ls = 0.0f;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][j]), ones, ls, false);
-    l_run += ls;
-    // O^T += V^T P^T: 4 steps of 16 keys; step ks takes keys 16*ks + hl*8 .. +8
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const uint4 u = make_uint4(pk[ks >> 1][(ks & 1) * 4 + 0], pk[ks >> 1][(ks & 1) * 4 + 1],
-                                 pk[ks >> 1][(ks & 1) * 4 + 2], pk[ks >> 1][(ks & 1) * 4 + 3]);
-      const bf16x8 pb = __builtin_bit_cast(bf16x8, u);
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(cur + vlane + dt * 32 * T::kPitchV + ks * 32);
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
-      }
-    }
   };
 
-  const int nsteps = (w.kv_hi - w.kv_lo + kKvStep - 1) / kKvStep;
-  load(w.kv_lo);
-  store(smem);
-  __syncthreads();
-
-  for (int it = 0; it < nsteps; ++it) {
-    const int kb = w.kv_lo + it * kKvStep;
-    const char* cur = smem + (it & 1) * T::kStage;
-    char* nxt = smem + ((it + 1) & 1) * T::kStage;
-    const bool more = it + 1 < nsteps;
-    if (more) load(kb + kKvStep);
-    if (kb <= pmax) {  // some row of this wave sees a key of this step
-      if (kb + kKvStep - 1 > pmin)
-        step(cur, kb, std::true_type{});
-      else
-        step(cur, kb, std::false_type{});
+  // One step j, scores of step j in sbuf[B] (masked, max applied):
+  //   block 1: QK of step j+1 into sbuf[1-B], interleaved with the weights of step j
+  //   block 2: PV of step j, interleaved with mask + max of step j+1
+  // The source order is fixed with scheduling fences so that every MFMA is
+  // followed by independent vector work of the other half of the pipeline.
+  auto fused = [&](auto bsel, auto mask_next, auto has_next, int j) {
+    constexpr int B = decltype(bsel)::value, NB = 1 - B;
+    constexpr bool kMaskNext = decltype(mask_next)::value;
+    constexpr bool kNext = decltype(has_next)::value;
+    const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    uint32_t pk[16];
+    float ls = 0.0f;
+    // block 1
+    bf16x8 ka[kQk];
+    if constexpr (kNext) {
+      ka[0] = kread(j + 1, 0);
+      ka[1] = kread(j + 1, 1);
     }
-    if (more) store(nxt);
-    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kQk; ++i) {
+      if constexpr (kNext) {
+        if (i + 2 < kQk) ka[i + 2] = kread(j + 1, i + 2);
+        const int kk = i >> 1, kt = i & 1;
+        if (kk == 0) {
+          const f32x16 zero = {};
+          sbuf[NB][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i], qf[0], zero, 0, 0, 0);
+        } else {
+          sbuf[NB][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i], qf[kk], sbuf[NB][kt], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kElPerQk; u += 2) {
+        const int e = i * kElPerQk + u;
+        pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][e >> 4][e & 15], c, nm)),
+                                 __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][(e + 1) >> 4][(e + 1) & 15], c, nm)));
+        // the row sum adds the same bf16-rounded weights that enter the PV
+        // product, so the normalised weights sum to one exactly
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l_run += ls;
+    // block 2
+    const int lim = pos - (w.kv_lo + (j + 1) * kKvStep) - hl * 8;
+    float mx = -__builtin_inff();
+    bf16x8 va[kPv];
+    va[0] = vread(j, 0);
+    va[1] = vread(j, 1);
+#pragma unroll
+    for (int i = 0; i < kPv; ++i) {
+      if (i + 2 < kPv) va[i + 2] = vread(j, i + 2);
+      const int ks = i / (D / 32), dt = i % (D / 32);
+      // P sub-step ks = keys 16*ks + hl*8 .. +8 = packed weights 4*ks .. 4*ks+3
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
+      oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pb, oacc[dt], 0, 0, 0);
+      if constexpr (kNext) {
+#pragma unroll
+        for (int u = 0; u < kElPerPv; ++u) {
+          const int e = i * kElPerPv + u;
+          float x = sbuf[NB][e >> 4][e & 15];
+          if constexpr (kMaskNext) {
+            x = ((e >> 4) * 32 + ((e & 15) >> 3) * 16 + (e & 7)) <= lim ? x : -__builtin_inff();
+            sbuf[NB][e >> 4][e & 15] = x;
+          }
+          mx = fmaxf(mx, x);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    mx_next = mx;
+  };
+
+  // Step s's K sits in K buffer s % 2 and its V in V buffer s % 2; in
+  // iteration j the copies of K_{j+2} and V_{j+1} are issued after the
+  // barrier that ended iteration j-1 (the buffers' previous contents K_j and
+  // V_{j-1} were last read before it) and waited for before the barrier that
+  // ends iteration j.
+  auto need_mask = [&](int s) { return w.kv_lo + s * kKvStep + kKvStep - 1 > pmin; };
+  // steps this wave computes: keys up to its largest position.  A wave past
+  // them still copies its share of every step and meets every barrier.
+  const int nw = pmax >= w.kv_lo ? min(n, (pmax - w.kv_lo) / kKvStep + 1) : 0;
+  issue(0, 0);
+  issue(1, -1);
+  wait_dma<0>();
+  lds_barrier();
+  if (nw > 0) {
+    qk_plain(0, 0);
+    if (need_mask(0)) max_plain(0, 0, std::true_type{}); else max_plain(0, 0, std::false_type{});
+    rescale();
+  }
+  lds_barrier();  // every wave is done with K_0 before K_2 replaces it
+
+  // Iterations run in two loops.  The first handles two steps per trip
+  // while both steps and their successors need no mask (the scores of step j
+  // alternate between sbuf[0] and sbuf[1], so a trip starts and ends with
+  // them in sbuf[0]).  The second handles the remaining steps (the diagonal
+  // ones and the last) one at a time, copying the next scores back to
+  // sbuf[0].  Waves may split their steps differently between the loops;
+  // every step still ends with exactly one barrier.
+  auto tail = [&](int j) {
+    if (j + 1 < nw) rescale();
+    wait_dma<0>();
+    lds_barrier();
+  };
+  int j = 0;
+  for (; j + 2 < nw && !need_mask(j + 2); j += 2) {
+    issue(j + 2, j + 1);
+    fused(std::integral_constant<int, 0>{}, std::false_type{}, std::true_type{}, j);
+    tail(j);
+    issue(j + 3, j + 2);
+    fused(std::integral_constant<int, 1>{}, std::false_type{}, std::true_type{}, j + 1);
+    tail(j + 1);
+  }
+  // Remaining steps (the diagonal ones and the last) run without overlap:
+  // weights of step j, PV of step j, then QK + mask + max of step j+1 into
+  // the same score registers.  Same copy schedule as the pipelined loop.
+  auto plain = [&](int jj) {
+    const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    uint32_t pk[16];
+    float ls = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 32; e += 2) {
+      pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[0][e >> 4][e & 15], c, nm)),
+                               __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[0][(e + 1) >> 4][(e + 1) & 15], c, nm)));
+      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
+    }
+    l_run += ls;
+#pragma unroll
+    for (int i = 0; i < kPv; ++i) {
+      const int ks = i / (D / 32), dt = i % (D / 32);
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
+      oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vread(jj, i), pb, oacc[dt], 0, 0, 0);
+    }
+    if (jj + 1 < nw) {
+      qk_plain(0, jj + 1);
+      if (need_mask(jj + 1)) max_plain(0, jj + 1, std::true_type{}); else max_plain(0, jj + 1, std::false_type{});
+    }
+  };
+  for (; j < n; ++j) {
+    issue(j + 2, j + 1);
+    if (j < nw) plain(j);
+    tail(j);
   }
 
   // epilogue: lane (hl, ln) holds row r, channels dt*32 + (i/4)*8 + hl*4 + i%4
@@ -308,7 +470,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
       for (int g4 = 0; g4 < 4; ++g4) {
         f32x4 v;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = oacc[dt][g4 * 4 + j] * inv;
+        for (int q = 0; q < 4; ++q) v[q] = oacc[dt][g4 * 4 + q] * inv;
         *reinterpret_cast<f32x4*>(orow + dt * 32 + g4 * 8 + hl * 4) = v;
       }
     if (hl == 0)
