@@ -216,8 +216,9 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   } else if (!(o.flags & MSA_PLAN_NO_AUTO_SPLIT) && !units.empty()) {
     double total_steps = 0;
     for (const Unit& u : units) total_steps += (double)(steps(u.kv_hi) + 1);
-    // aim at >= 2 work items per workgroup slot for the longest units
-    const int64_t share = (int64_t)std::ceil(total_steps / (2.0 * slots_total)) * kKvStep;
+    // aim at about 3 work items per workgroup slot: a unit longer than this
+    // share of the total is cut into pieces no longer than the share
+    const int64_t share = (int64_t)std::ceil(total_steps / (3.0 * slots_total)) * kKvStep;
     split_keys = std::max<int64_t>(kMinSplitKeys, share);
   }
   struct Piece {
@@ -229,9 +230,7 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     const Unit& u = units[ui];
     int64_t nsplit = 1;
     if (split_keys > 0) {
-      // auto mode splits only units clearly longer than the share
-      const bool forced = o.kv_split_tokens > 0;
-      if (forced ? (u.kv_hi > split_keys) : (u.kv_hi > 2 * split_keys))
+      if (u.kv_hi > split_keys)
         nsplit = (u.kv_hi + split_keys - 1) / split_keys;
     }
     if (nsplit <= 1) {
