@@ -316,3 +316,16 @@ def test_plan_reuse_across_layers_and_streams(oracle_lib):
         ro, _ = oracle_lib.forward(ii)
         mx, mean = errors(bf16_to_f32(o), ro)
         assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
+@pytest.mark.parametrize("hq,hkv,d,tile", [(64, 2, 128, 0), (64, 2, 64, msa.MSA_PLAN_TILE_ROWS_128),
+                                           (128, 1, 64, 0), (128, 1, 128, msa.MSA_PLAN_TILE_ROWS_128),
+                                           (256, 1, 64, 0)])
+def test_large_query_groups(oracle_lib, hq, hkv, d, tile):
+    """G = Hq/Hkv of 32, 128 and 256: a tile holds 128/G or 256/G tokens
+    (one token per tile at G = 256, which needs the 256-row form)."""
+    inst = workloads.make_random(301 + hq + d, num_seqs=2, num_q_heads=hq, num_kv_heads=hkv,
+                                 head_dim=d, max_len=300, max_segs=3, keep_logical=False)
+    _, _, plan = check_full(inst, oracle_lib, flags=tile)
+    expect = 128 if tile == msa.MSA_PLAN_TILE_ROWS_128 else (256 if hq // hkv > 128 else plan.info()["tile_rows"])
+    assert plan.info()["tile_rows"] == expect
