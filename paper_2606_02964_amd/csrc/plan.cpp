@@ -18,8 +18,10 @@
 //   4. key splits: units much longer than the average share of a workgroup
 //      slot are cut into 64-aligned key ranges, merged later by log-sum-exp;
 //   5. order: (sequence, KV head) groups are spread over the 8 XCDs (blockIdx
-//      i runs on XCD i % 8) so tiles sharing K/V share one XCD's L2, longest
-//      first inside each XCD.
+//      i runs on XCD i % 8) so tiles sharing K/V share one XCD's L2.  Inside
+//      each XCD, groups start in decreasing order of their longest piece and
+//      a group's pieces run back to back, longest first, so that no long
+//      piece (a decode row over a long context) is left for the end.
 #include "plan.h"
 
 #include <algorithm>
@@ -282,7 +284,7 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     ghome[(size_t)gi] = x;
     load[(size_t)x] += gcost[(size_t)gi];
   }
-  // pieces sorted: by group cost (desc), then own cost (desc), then index
+  // pieces in XCD-assignment order: by group cost (desc), then own cost (desc), then index
   std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
     const Unit& ua = units[(size_t)pieces[(size_t)a].unit];
     const Unit& ub = units[(size_t)pieces[(size_t)b].unit];
@@ -302,6 +304,26 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     }
     queue[(size_t)x].push_back(pi);
   }
+  // Inside each XCD: groups by decreasing longest piece, then by id; pieces
+  // of one group stay adjacent, longest first.  Ordering by total group cost
+  // alone would leave a light group's long piece to run last.
+  std::vector<double> gmax((size_t)ngroups, 0.0);
+  for (const Piece& p : pieces) {
+    const Unit& u = units[(size_t)p.unit];
+    double& m = gmax[(size_t)((int64_t)u.seq * Hkv + u.kv_head)];
+    m = std::max(m, pcost(p));
+  }
+  for (auto& qx : queue)
+    std::stable_sort(qx.begin(), qx.end(), [&](int32_t a, int32_t b) {
+      const Piece& pa = pieces[(size_t)a];
+      const Piece& pb = pieces[(size_t)b];
+      const Unit& ua = units[(size_t)pa.unit];
+      const Unit& ub = units[(size_t)pb.unit];
+      const int64_t ga = (int64_t)ua.seq * Hkv + ua.kv_head, gb = (int64_t)ub.seq * Hkv + ub.kv_head;
+      if (gmax[(size_t)ga] != gmax[(size_t)gb]) return gmax[(size_t)ga] > gmax[(size_t)gb];
+      if (ga != gb) return ga < gb;
+      return pcost(pa) > pcost(pb);
+    });
   size_t rounds = 0;
   for (const auto& q : queue) rounds = std::max(rounds, q.size());
   // trim trailing XCDs with nothing in the last round so a small problem

@@ -411,6 +411,43 @@ def test_fused_ablation_layouts():
                 assert suf[0] == (0, ctx - 128 - cached)
 
 
+def _xcd_queues(work):
+    """Work item i runs on XCD i % 8: per XCD, the (group, keys) of its items
+    in launch order (padding items skipped)."""
+    queues = [[] for _ in range(8)]
+    for i, w in enumerate(work):
+        if int(w[3]) > 0:
+            queues[i % 8].append(((int(w[0]), int(w[1])), (int(w[5]) - int(w[4]) + 63) // 64))
+    return queues
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 5])
+def test_xcd_queue_order(msa, cfg):
+    """Inside each XCD queue, (sequence, KV head) groups start in decreasing
+    order of their longest piece, a group's pieces are adjacent and run
+    longest first.  On the mixed workload this puts the decode rows over the
+    longest contexts ahead of the prefill groups with shorter pieces."""
+    inst = make_layout_only(cfg)
+    _, work, _ = msa.msa_plan_export(host_plan(msa, inst))
+    for q in _xcd_queues(work):
+        longest = {}
+        for g, n in q:
+            longest[g] = max(longest.get(g, 0), n)
+        seen, prev_g, prev_n = set(), None, None
+        for g, n in q:
+            if g != prev_g:
+                assert g not in seen, "a group's pieces are not adjacent"
+                if prev_g is not None:
+                    assert longest[g] <= longest[prev_g]
+                seen.add(g)
+            else:
+                assert n <= prev_n
+            prev_g, prev_n = g, n
+    if cfg == 5:
+        # every queue's first piece is the longest piece of that queue
+        assert all(q[0][1] == max(n for _, n in q) for q in _xcd_queues(work) if q)
+
+
 def test_tile_width_choice(msa):
     """Wide (256-row) tiles for plans with many tiles, narrow (128-row) tiles
     for small and decode-only plans; flags force either."""
