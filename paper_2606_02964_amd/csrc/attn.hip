@@ -4,7 +4,7 @@
 // per wave) per work item: query rows of one sequence sharing one KV head,
 // over one key range.  Each 64-key step:
 //   - paged gather: the step's 4 cache blocks are looked up in the block
-//     table and copied straight into LDS (global_load_lds, 16 bytes a lane,
+//     table (scalar loads) and copied straight into LDS (global_load_lds, 16 bytes a lane,
 //     no staging registers): K as [key][d] rows, V as the cache's
 //     channel-major [d][16 keys] pages, 16-byte chunks XOR-swizzled so that
 //     every operand read is free of bank conflicts.  K runs one step ahead of
@@ -104,6 +104,15 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// scalar load of one wave-uniform int32 (through the scalar cache, waited
+// for at once); the compiler only emits vector loads here because the
+// global->LDS copies count as possible writes to global memory
+__device__ __forceinline__ int32_t sload_i32(const int32_t* a) {
+  int32_t v;
+  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(a) : "memory");
+  return v;
+}
+
 // running-max threshold of the lazy rescale: the reference max only moves
 // when a row's max grows by more than this (log2 units), so the unnormalised
 // weights stay <= 2^8
@@ -184,8 +193,8 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   // A step has 8 pages: the K and the V page of each of its 4 blocks (page
   // pg: block pg & 3, V if pg >= 4); wave w copies pages w, w + W, ...
   // issue(sk, sv) copies the K pages of step sk and the V pages of step sv
-  // (-1: none).  All block ids are read before the first copy, so no id load
-  // waits behind copies of the same call.  A block at or past kv_hi is not
+  // (-1: none).  All block ids are read (scalar loads) before the first
+  // copy, so no id load waits behind copies.  A block at or past kv_hi is not
   // read; its V page is zero-filled instead (its K page keeps old values:
   // those keys are masked by selection, so never meet arithmetic).
   constexpr int kPagesPerWave = 8 / W;
@@ -201,7 +210,8 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
       const int kb = w.kv_lo + st * kKvStep;
       have[k] = live && kb + bi * kBlockSize < w.kv_hi;
       zero[k] = live && !have[k] && pg >= 4;
-      ids[k] = have[k] ? (int64_t)__builtin_amdgcn_readfirstlane(bt[(kb >> 4) + bi]) : 0;
+      ids[k] = 0;
+      if (have[k]) ids[k] = (int64_t)sload_i32(bt + (kb >> 4) + bi);
     }
 #pragma unroll
     for (int k = 0; k < kPagesPerWave; ++k) {
