@@ -88,9 +88,18 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // 16 bytes per lane from global memory straight into LDS at
-// lds + 16 * lane (a wave copies 1 KB); completion is tracked by vmcnt
+// lds + 16 * lane (a wave copies 1 KB; M0 holds the wave's LDS base);
+// completion is tracked by vmcnt.  Issued as inline assembly: when the
+// compiler sees these copies it treats the LDS counter as unordered and
+// waits for every outstanding LDS read (lgkmcnt(0)) before each MFMA, which
+// cancels the operand read-ahead.  The kernel itself waits for the copies
+// (wait_dma) before the barrier that publishes them; the compiler's own
+// vmcnt waits stay correct because vector loads complete in issue order,
+// so extra loads it does not count only make those waits stricter.  The
+// s_nop covers the M0-write-to-LDS-DMA hazard.
 __device__ __forceinline__ void dma16(const void* g, void* lds) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void_t*)lds, 16, 0, 0);
+  const uint32_t l = (uint32_t)(uintptr_t)(lds_void_t*)lds;
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(l) : "memory");
 }
 // wait until at most n copies issued by this wave are outstanding
 template <int n>
@@ -250,6 +259,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   constexpr int kPv = 4 * (D / 32);                   // PV MFMAs per step, ordered (ks, dt)
   constexpr int kElPerQk = 32 / kQk;                  // scores handled per QK MFMA
   constexpr int kElPerPv = 32 / kPv;                  // scores handled per PV MFMA
+  constexpr int kAhead = 3;                           // operand reads issued ahead of their MFMA
 
   // K operand of QK MFMA i of step s (register i of a lane: key row kt*32 + krow_m)
   auto kread = [&](int s, int i) -> bf16x8 {
@@ -323,13 +333,13 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
     // block 1
     bf16x8 ka[kQk];
     if constexpr (kNext) {
-      ka[0] = kread(j + 1, 0);
-      ka[1] = kread(j + 1, 1);
+#pragma unroll
+      for (int a = 0; a < kAhead; ++a) ka[a] = kread(j + 1, a);
     }
 #pragma unroll
     for (int i = 0; i < kQk; ++i) {
       if constexpr (kNext) {
-        if (i + 2 < kQk) ka[i + 2] = kread(j + 1, i + 2);
+        if (i + kAhead < kQk) ka[i + kAhead] = kread(j + 1, i + kAhead);
         const int kk = i >> 1, kt = i & 1;
         if (kk == 0) {
           const f32x16 zero = {};
@@ -354,11 +364,11 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
     const int lim = pos - (w.kv_lo + (j + 1) * kKvStep) - hl * 8;
     float mx = -__builtin_inff();
     bf16x8 va[kPv];
-    va[0] = vread(j, 0);
-    va[1] = vread(j, 1);
+#pragma unroll
+    for (int a = 0; a < kAhead; ++a) va[a] = vread(j, a);
 #pragma unroll
     for (int i = 0; i < kPv; ++i) {
-      if (i + 2 < kPv) va[i + 2] = vread(j, i + 2);
+      if (i + kAhead < kPv) va[i + kAhead] = vread(j, i + kAhead);
       const int ks = i / (D / 32), dt = i % (D / 32);
       // P sub-step ks = keys 16*ks + hl*8 .. +8 = packed weights 4*ks .. 4*ks+3
       const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
