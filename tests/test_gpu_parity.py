@@ -161,6 +161,32 @@ def test_named_workload_sampled_parity(oracle_lib, cfg):
     assert float(np.abs(lsel - rl).max()) <= LSE_ABS
 
 
+def test_longest_context_sampled_parity(oracle_lib):
+    """Llama 3.1's longest context, 131072 keys, at one tensor-parallel
+    rank's share of Llama-3.1-8B (8 query heads, 2 KV heads): a 1024-token
+    chunk at the end and a 512-token recompute segment in the middle of one
+    sequence, plus a decode row over 100000 keys in a second one.  The
+    automatic plan splits these long units; sampled (row, head) items against
+    the oracle, and the first and last row of every segment."""
+    L = 131072
+    segs = [[(65536, 512), (L - 1024, 1024)], [(99999, 1)]]
+    inst = workloads.make_layout(41, [L, 100000], segs, 8, 2, 128, keep_logical=False)
+    o, lse, plan = run(DeviceInstance(inst))
+    assert plan.info()["num_merge"] > 0, "expected key splits on 131072-key units"
+    go = o.float()
+    assert torch.isfinite(go).all().item() and torch.isfinite(lse).all().item()
+    rows, heads = _sample_items(inst, 120, seed=41)
+    edges = np.array([0, 511, 512, 1535, inst.total_q - 1], dtype=np.int64)
+    rows = np.r_[rows, edges]
+    heads = np.r_[heads, np.arange(edges.size, dtype=np.int32) * 3 % 8].astype(np.int32)
+    ro, rl = oracle_lib.forward(inst, rows=rows, heads=heads)
+    gsel = go[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    mx, mean = errors(gsel, ro)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
+    lsel = lse[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    assert float(np.abs(lsel - rl).max()) <= LSE_ABS
+
+
 def test_config4_forced_split_matches_unsplit(oracle_lib):
     inst = workloads.make_config(4)
     d = DeviceInstance(inst)
