@@ -16,6 +16,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -36,10 +37,16 @@ def log(*a):
 
 
 def kernel_hash() -> str:
+    """Hash of the attention kernel's source code with comments and blank
+    lines removed, so that counter figures stay attached to the code they
+    were taken on and survive comment edits."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p), encoding="utf-8") as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", "", src)
+        h.update("\n".join(l.strip() for l in src.splitlines() if l.strip()).encode())
     return h.hexdigest()[:16]
 
 

@@ -4,11 +4,12 @@
 // per wave) per work item: query rows of one sequence sharing one KV head,
 // over one key range.  Each 64-key step:
 //   - paged gather: the step's 4 cache blocks are looked up in the block
-//     table (scalar loads) and copied straight into LDS (global_load_lds, 16 bytes a lane,
-//     no staging registers): K as [key][d] rows, V as the cache's
-//     channel-major [d][16 keys] pages, 16-byte chunks XOR-swizzled so that
-//     every operand read is free of bank conflicts.  K runs one step ahead of
-//     V in rings of two stages;
+//     table (scalar loads) and copied straight into LDS (global_load_lds,
+//     16 bytes a lane, no staging registers): K as [key][d] rows, V as the
+//     cache's channel-major [d][16 keys] pages, 16-byte chunks XOR-swizzled
+//     so that every operand read is free of bank conflicts.  K runs one step
+//     ahead of V in rings of two stages.  The block-id loads and the copies
+//     are inline assembly (see sload_i32 and dma16 for why);
 //   - S^T = K Q^T on v_mfma_f32_32x32x16_bf16.  K is the A operand, so each
 //     lane holds one query row (a column of S^T) and 16 of the 32 keys: the
 //     row max and row sum need one exchange with the lane 32 apart only;
