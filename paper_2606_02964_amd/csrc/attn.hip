@@ -61,7 +61,6 @@ template <int D>
 struct Tile {
   static constexpr int kBytesK = kKvStep * D * 2;
   static constexpr int kBytesV = kKvStep * D * 2;
-  static constexpr int kStage = kBytesK + kBytesV;
   static constexpr int kPage = kBlockSize * D * 2;  // bytes of one block of K or V
   static constexpr int kDmaPerPage = kPage / 1024;  // 1 KB per wave-wide 16-byte copy
 };
