@@ -355,3 +355,49 @@ def test_large_query_groups(oracle_lib, hq, hkv, d, tile):
     _, _, plan = check_full(inst, oracle_lib, flags=tile)
     expect = 128 if tile == msa.MSA_PLAN_TILE_ROWS_128 else (256 if hq // hkv > 128 else plan.info()["tile_rows"])
     assert plan.info()["tile_rows"] == expect
+
+
+def test_hip_graph_replays_match_eager():
+    """msa_kv_append and msa_forward (with key splits, so the merge kernel
+    runs too) allocate and clear nothing, so a serving loop can capture them
+    in a HIP graph.  Every replay, with eager work and synchronisation in
+    between, must give the eager outputs bit for bit."""
+    inst = workloads.make_random(211, num_seqs=3, num_q_heads=16, num_kv_heads=4, head_dim=128,
+                                 max_len=1500, max_segs=5, keep_logical=False)
+    d = DeviceInstance(inst)
+    plan = d.plan(kv_split_tokens=256)
+    info = plan.info()
+    assert info["num_merge"] > 0
+    kn, vn = (dev_bf16(x) for x in workloads.make_fresh_kv(inst, 5))
+    shape_o = (inst.total_q, inst.num_q_heads, inst.head_dim)
+    ws = torch.empty(info["workspace_bytes"], dtype=torch.uint8, device="cuda")
+
+    def step(o, lse):
+        msa.msa_kv_append(plan, kn, vn, d.bt, d.k, d.v)
+        msa.msa_forward(plan, d.q, d.k, d.v, d.bt, o, lse, ws)
+
+    o_ref = torch.empty(shape_o, dtype=torch.bfloat16, device="cuda")
+    l_ref = torch.empty(shape_o[:2], dtype=torch.float32, device="cuda")
+    step(o_ref, l_ref)
+    torch.cuda.synchronize()
+
+    o = torch.empty_like(o_ref)
+    lse = torch.empty_like(l_ref)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up on the capture stream
+        step(o, lse)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(o, lse)
+    for rep in range(4):
+        o.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o.view(torch.int16), o_ref.view(torch.int16)), rep
+        assert torch.equal(lse.view(torch.int32), l_ref.view(torch.int32)), rep
+        (d.q.float() * 2).sum().item()  # unrelated eager work between replays
