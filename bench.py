@@ -518,7 +518,7 @@ def main():
             times.append(a.elapsed_time(b))
         cold_ms = float(np.median(times))
         del flush
-        log(f"cold: {cold_ms * 1e3:.1f} us/call (median)")
+        log(f"cold: {cold_ms * 1e3:.1f} us/call (median of " + " ".join(f"{t * 1e3:.0f}" for t in times) + ")")
 
     useful = info["useful_flops"]
     achieved = useful / (ms * 1e-3) / 1e12
