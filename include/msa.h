@@ -104,9 +104,11 @@ typedef struct msa_plan_opts {
 #define MSA_PLAN_NO_AUTO_SPLIT 2
 /* Force the tile width (query rows x heads per workgroup).  Without either
  * flag the planner takes 256-row tiles (one workgroup per CU; each K/V step
- * is loaded once for twice the rows) when the plan has many tiles, and
- * 128-row tiles (two workgroups per CU, more concurrent key streams) for
- * small and decode-heavy plans.  The two flags are exclusive. */
+ * is loaded once for twice the rows) when the plan has many tiles and a
+ * long run of key steps per workgroup slot, and 128-row tiles (two
+ * workgroups per CU: one's start-up and tail overlap the other's work, more
+ * concurrent key streams) for small, short and decode-heavy plans.  The two
+ * flags are exclusive. */
 #define MSA_PLAN_TILE_ROWS_128 4
 #define MSA_PLAN_TILE_ROWS_256 8
 

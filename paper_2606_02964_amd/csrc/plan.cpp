@@ -11,9 +11,10 @@
 //      across segment gaps as long as the keys masked for the earlier rows
 //      stay a small fraction of the tile's work.  tile_rows is 256 (one
 //      workgroup per CU, each K/V step loaded once for 256 rows) when the
-//      plan has enough tiles to fill the GPU several times over, else 128
-//      (two workgroups per CU, more concurrent key streams for small and
-//      decode-heavy plans);
+//      128-row tiling has many tiles and a long run of key steps per
+//      workgroup slot, else 128 (two workgroups per CU: one's start-up and
+//      tail overlap the other's work, and decode-heavy plans keep more key
+//      streams in flight);
 //   3. units: tile x KV head, keys [0, max position in tile + 1);
 //   4. key splits: units much longer than the average share of a workgroup
 //      slot are cut into 64-aligned key ranges, merged later by log-sum-exp;
@@ -35,6 +36,11 @@ namespace {
 constexpr int kXcds = 8;
 constexpr int kCUs = 256;
 constexpr int64_t kWideMinTiles = 1024;  // narrow tiles from which wide tiles pay
+// 64-key steps per workgroup slot of the narrow tiling from which wide tiles
+// pay: shorter plans gain more from two workgroups per CU (one's start-up
+// and tail overlap the other's work) than from loading each K/V step once
+// for 256 rows (measured crossover about 400 steps per slot)
+constexpr double kWideMinStepsPerSlot = 384.0;
 constexpr double kWasteFrac = 0.125;     // masked keys allowed per tile, relative
 constexpr int64_t kMinSplitKeys = 1024;  // never split below this many keys
 
@@ -145,18 +151,54 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
       for (int32_t k = seg_indptr[b]; k < seg_indptr[b + 1]; ++k)
         for (int32_t t = 0; t < seg_len[k]; ++t) P.row_pos[(size_t)r++] = seg_start[k] + t;
   }
-  // tile width: forced by a flag, else wide when the narrow tiling would
-  // give enough tiles (counted without the splits at segment gaps)
+  // 2. tiles of up to `tt` consecutive tokens of one sequence, packed
+  // across segment gaps while the keys masked for the earlier rows stay a
+  // small part of the tile's work; one unit per tile and KV head
+  auto make_units = [&](int32_t tt) {
+    std::vector<Unit> units;
+    for (int32_t b = 0; b < B; ++b) {
+      const int64_t lo = seq_row0[b], hi = seq_row0[b + 1];
+      int64_t i = lo;
+      while (i < hi) {
+        const int64_t first = i;
+        double useful = (double)P.row_pos[(size_t)i] + 1.0, waste = 0.0;
+        int32_t cnt = 1;
+        ++i;
+        while (i < hi && cnt < tt) {
+          const double step = (double)P.row_pos[(size_t)i] - (double)P.row_pos[(size_t)(i - 1)];
+          const double nw = waste + cnt * step;
+          const double nu = useful + (double)P.row_pos[(size_t)i] + 1.0;
+          if (nw > kWasteFrac * nu && nw > (double)kKvStep * tt) break;
+          waste = nw;
+          useful = nu;
+          ++cnt;
+          ++i;
+        }
+        const int32_t kv_hi = P.row_pos[(size_t)(first + cnt - 1)] + 1;
+        for (int32_t g = 0; g < s.num_kv_heads; ++g) units.push_back(Unit{b, g, (int32_t)first, cnt, kv_hi});
+      }
+    }
+    return units;
+  };
+
+  // tile width: forced by a flag, else wide when the narrow tiling has many
+  // tiles and enough work per workgroup slot (G > 128 needs wide tiles)
+  const int32_t narrow_tokens = G <= kTileRowsNarrow ? kTileRowsNarrow / G : 0;
+  std::vector<Unit> narrow_units;
   {
     int32_t rows = kTileRowsNarrow;
     if (o.flags & MSA_PLAN_TILE_ROWS_256) {
       rows = kTileRowsWide;
     } else if (!(o.flags & MSA_PLAN_TILE_ROWS_128)) {
-      const int64_t tok = kTileRowsNarrow / std::max<int32_t>(1, std::min<int32_t>(G, kTileRowsNarrow));
-      int64_t narrow = 0;
-      for (int32_t b = 0; b < B; ++b) narrow += (seq_row0[b + 1] - seq_row0[b] + tok - 1) / tok;
-      narrow *= s.num_kv_heads;
-      if (G > kTileRowsNarrow || narrow >= kWideMinTiles) rows = kTileRowsWide;
+      if (G > kTileRowsNarrow) {
+        rows = kTileRowsWide;
+      } else {
+        narrow_units = make_units(narrow_tokens);
+        double steps = 0;
+        for (const Unit& u : narrow_units) steps += (double)((u.kv_hi + kKvStep - 1) / kKvStep);
+        if ((int64_t)narrow_units.size() >= kWideMinTiles && steps >= kWideMinStepsPerSlot * 2.0 * kCUs)
+          rows = kTileRowsWide;
+      }
     }
     P.tile_rows = rows;
     P.tile_tokens = rows / G;
@@ -183,31 +225,10 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
       }
   }
 
-  // 2-3. tiles and units
-  std::vector<Unit> units;
+  // 3. units of the chosen width
+  std::vector<Unit> units = narrow_units.empty() || tile_tokens != narrow_tokens ? make_units(tile_tokens)
+                                                                                : std::move(narrow_units);
   const int32_t Hkv = s.num_kv_heads, d = s.head_dim;
-  for (int32_t b = 0; b < B; ++b) {
-    const int64_t lo = seq_row0[b], hi = seq_row0[b + 1];
-    int64_t i = lo;
-    while (i < hi) {
-      const int64_t first = i;
-      double useful = (double)P.row_pos[(size_t)i] + 1.0, waste = 0.0;
-      int32_t cnt = 1;
-      ++i;
-      while (i < hi && cnt < tile_tokens) {
-        const double step = (double)P.row_pos[(size_t)i] - (double)P.row_pos[(size_t)(i - 1)];
-        const double nw = waste + cnt * step;
-        const double nu = useful + (double)P.row_pos[(size_t)i] + 1.0;
-        if (nw > kWasteFrac * nu && nw > (double)kKvStep * tile_tokens) break;
-        waste = nw;
-        useful = nu;
-        ++cnt;
-        ++i;
-      }
-      const int32_t kv_hi = P.row_pos[(size_t)(first + cnt - 1)] + 1;
-      for (int32_t g = 0; g < Hkv; ++g) units.push_back(Unit{b, g, (int32_t)first, cnt, kv_hi});
-    }
-  }
   P.num_tiles = (int64_t)units.size();
 
   // 4. key splits
@@ -253,7 +274,7 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   P.num_slots = slots;
   P.workspace_bytes = slots * slot_floats(d, P.tile_rows) * (int64_t)sizeof(float);
 
-  // 5. order: groups (seq, kv head) -> XCD queues, longest first
+  // 5. order: groups (seq, kv head) -> XCD queues
   const int64_t ngroups = (int64_t)B * Hkv;
   std::vector<double> gcost((size_t)ngroups, 0.0);
   auto pcost = [&](const Piece& p) { return (double)(steps(p.hi - p.lo) + 1); };

@@ -448,12 +448,40 @@ def test_xcd_queue_order(msa, cfg):
         assert all(q[0][1] == max(n for _, n in q) for q in _xcd_queues(work) if q)
 
 
+def _descriptors(kv_lens, segs, hq, hkv, d):
+    """Plan descriptors of a layout, without drawing its tensors."""
+    class L:
+        pass
+    inst = L()
+    inst.num_seqs, inst.num_q_heads, inst.num_kv_heads, inst.head_dim = len(kv_lens), hq, hkv, d
+    inst.scale = 1.0 / np.sqrt(d)
+    inst.seq_kv_len = np.asarray(kv_lens, np.int32)
+    inst.seg_start = np.asarray([st for sg in segs for (st, n) in sg], np.int32)
+    inst.seg_len = np.asarray([n for sg in segs for (st, n) in sg], np.int32)
+    inst.seg_indptr = np.cumsum([0] + [len(sg) for sg in segs]).astype(np.int32)
+    inst.max_blocks_per_seq = max(-(-x // 16) for x in kv_lens)
+    inst.num_blocks = sum(-(-x // 16) for x in kv_lens)
+    return inst
+
+
 def test_tile_width_choice(msa):
-    """Wide (256-row) tiles for plans with many tiles, narrow (128-row) tiles
-    for small and decode-only plans; flags force either."""
+    """Wide (256-row) tiles for plans with many tiles and a long run of key
+    steps per workgroup slot; narrow (128-row) tiles for small, short and
+    decode-only plans; flags force either."""
     for cfg, rows in ((1, 128), (2, 256), (3, 256), (4, 256), (5, 256)):
         assert host_plan(msa, make_layout_only(cfg)).info()["tile_rows"] == rows, cfg
-    decode = workloads.make_config(5, decode_only=True)
+    # many narrow tiles, little work per slot: 8 x 1024-token requests whose
+    # first 896 tokens and last 128 are computed (2048 narrow tiles, ~34
+    # steps per slot) stay narrow; the same layout at 10240 tokens goes wide
+    for ctx, rows in ((1024, 128), (10240, 256)):
+        segs = workloads.fused_ablation_layout(ctx, 0, "suffix")
+        inst = _descriptors([ctx] * 8, [segs] * 8, 32, 8, 128)
+        assert host_plan(msa, inst).info()["tile_rows"] == rows, ctx
+    _, layout = workloads.CONFIGS[5]
+    lens, segs, heads = layout(np.random.Generator(np.random.PCG64(5)))
+    keep = [b for b in range(len(lens)) if segs[b] == [(lens[b] - 1, 1)]]  # the decode rows
+    decode = _descriptors([lens[b] for b in keep], [segs[b] for b in keep], heads["num_q_heads"],
+                          heads["num_kv_heads"], heads["head_dim"])
     assert host_plan(msa, decode).info()["tile_rows"] == 128
     assert host_plan(msa, decode, flags=msa.MSA_PLAN_TILE_ROWS_256).info()["tile_rows"] == 256
     assert host_plan(msa, make_layout_only(2), flags=msa.MSA_PLAN_TILE_ROWS_128).info()["tile_rows"] == 128
