@@ -497,3 +497,79 @@ def test_one_hip_runtime_per_process():
     out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
                          check=True).stdout.strip()
     assert out == "1", out
+
+
+C_CONSUMER = r"""
+#include <stdio.h>
+#include <string.h>
+#include "msa.h"
+#include "msa_evictor.h"
+
+int main(void) {
+  /* two sequences: [40, 72) of 100 keys; [0, 16) and [33, 34) of 50 keys */
+  const int32_t kv[2] = {100, 50}, indptr[3] = {0, 1, 3};
+  const int32_t start[3] = {40, 0, 33}, len[3] = {32, 16, 1};
+  msa_shape s;
+  memset(&s, 0, sizeof s);
+  s.num_seqs = 2; s.num_q_heads = 8; s.num_kv_heads = 2; s.head_dim = 128; s.block_size = 16;
+  s.max_blocks_per_seq = 7; s.num_blocks = 11; s.scale = 0.0883883476f;
+  s.q_stride_tok = 8 * 128; s.q_stride_head = 128; s.o_stride_tok = 8 * 128; s.o_stride_head = 128;
+  s.k_stride_block = 2 * 16 * 128; s.k_stride_head = 16 * 128; s.k_stride_tok = 128;
+  s.v_stride_block = 2 * 128 * 16; s.v_stride_head = 128 * 16; s.v_stride_dim = 16;
+  msa_plan_opts o;
+  memset(&o, 0, sizeof o);
+  o.flags = MSA_PLAN_HOST_ONLY;
+  msa_plan_t plan = NULL;
+  if (msa_plan(&s, kv, indptr, start, len, &o, NULL, &plan) != MSA_OK) {
+    printf("plan failed: %s\n", msa_last_error());
+    return 1;
+  }
+  msa_plan_info_t info;
+  if (msa_plan_info(plan, &info) != MSA_OK) return 2;
+  int32_t row_pos[49];
+  if (msa_plan_export(plan, row_pos, NULL, NULL) != MSA_OK) return 3;
+  printf("%lld %lld %lld %lld %d %d %d\n", (long long)info.total_q, (long long)info.num_tiles,
+         (long long)info.tile_rows, (long long)info.num_work, row_pos[0], row_pos[32], row_pos[48]);
+  /* a malformed plan reports through msa_last_error */
+  s.head_dim = 96;
+  msa_plan_t bad = NULL;
+  const msa_status st = msa_plan(&s, kv, indptr, start, len, &o, NULL, &bad);
+  printf("%d %d\n", (int)st, bad == NULL);
+  msa_plan_destroy(plan);
+
+  msa_evictor_params p;
+  memset(&p, 0, sizeof p);
+  p.alpha = 10.0; p.beta = 1.0; p.tau0 = 9.0; p.lambda = 1.0;
+  msa_evictor_t ev = NULL;
+  if (msa_evictor_create(&p, &ev) != MSA_OK) return 4;
+  msa_evictor_add(ev, 0, 0.0, 3.0);
+  msa_evictor_add(ev, 1, 5.0, 1.0);
+  int64_t id = -1;
+  msa_evictor_evict(ev, 6.0, &id);
+  printf("%lld %lld\n", (long long)id, (long long)msa_evictor_size(ev));
+  msa_evictor_destroy(ev);
+  return 0;
+}
+"""
+
+
+def test_plain_c_consumer(msa, tmp_path):
+    """The headers compile as strict C11 and a C program linked against the
+    library plans (host only), reports errors and drives the evictor, with
+    the same results as the Python binding."""
+    src = tmp_path / "consumer.c"
+    exe = tmp_path / "consumer"
+    src.write_text(C_CONSUMER)
+    libdir = os.path.dirname(msa.LIB_PATH)
+    subprocess.check_call(["gcc", "-std=c11", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                           "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe),
+                           "-L", libdir, "-lmsa", f"-Wl,-rpath,{libdir}"])
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    inst = _descriptors([100, 50], [[(40, 32)], [(0, 16), (33, 1)]], 8, 2, 128)
+    plan = host_plan(msa, inst)
+    info = plan.info()
+    row_pos, _, _ = msa.msa_plan_export(plan)
+    assert out[0].split() == [str(x) for x in (info["total_q"], info["num_tiles"], info["tile_rows"],
+                                                info["num_work"], row_pos[0], row_pos[32], row_pos[48])]
+    assert out[1].split() == [str(msa.MSA_ERR_UNSUPPORTED), "1"]
+    assert out[2].split() == ["1", "1"]  # Eq. 9 example: B (released at 5, cost 1) goes first at t = 6
