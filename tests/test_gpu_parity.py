@@ -187,6 +187,31 @@ def test_longest_context_sampled_parity(oracle_lib):
     assert float(np.abs(lsel - rl).max()) <= LSE_ABS
 
 
+def test_large_decode_batch_sampled_parity(oracle_lib):
+    """1024 sequences with one decode row each (contexts 64..2048 keys, one
+    TP=4 rank of Llama-3.1-8B: 8 query heads, 2 KV heads), plus 4 prefill
+    chunks: thousands of work items, narrow tiles, automatic splits.
+    Sampled (row, head) items and every sequence's row for head 0 against
+    the oracle."""
+    rng = np.random.Generator(np.random.PCG64(43))
+    lens = [int(x) for x in rng.integers(64, 2049, size=1024)]
+    segs = [[(L - 1, 1)] for L in lens]
+    for b in (3, 500, 777, 1023):
+        segs[b] = [(lens[b] - min(lens[b], 200), min(lens[b], 200))]
+    inst = workloads.make_layout(43, lens, segs, 8, 2, 128, keep_logical=False)
+    o, lse, plan = run(DeviceInstance(inst))
+    assert plan.info()["num_work"] > 1000
+    go = o.float()
+    assert torch.isfinite(go).all().item() and torch.isfinite(lse).all().item()
+    rows, heads = _sample_items(inst, 300, seed=43)
+    ro, rl = oracle_lib.forward(inst, rows=rows, heads=heads)
+    gsel = go[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    mx, mean = errors(gsel, ro)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
+    lsel = lse[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    assert float(np.abs(lsel - rl).max()) <= LSE_ABS
+
+
 def test_config4_forced_split_matches_unsplit(oracle_lib):
     inst = workloads.make_config(4)
     d = DeviceInstance(inst)
