@@ -1,12 +1,12 @@
 """Moving seeded instances to the GPU and running the HIP path through the
-C ABI (via the thin binding).  GPU-only; imported by ``-m gpu`` tests, the
-smoke check and the benchmark."""
+C ABI (via the thin binding).  GPU-only; imported by the ``-m gpu`` tests."""
 from __future__ import annotations
 
 import numpy as np
 import torch
 
 import paper_2606_02964_amd as msa
+from tolerance import LSE_ABS, MAX_ABS, MEAN_ABS, errors, raw_max_abs  # noqa: F401  (re-exported)
 
 
 def dev_bf16(bits: np.ndarray, device="cuda") -> torch.Tensor:
@@ -57,17 +57,3 @@ def run(dinst: DeviceInstance, plan=None, with_lse=True, sync=True, **plan_kw):
         torch.cuda.synchronize()
     return o, lse, plan
 
-
-def errors(gpu_o: np.ndarray, ref_o: np.ndarray):
-    d = np.abs(gpu_o.astype(np.float64) - ref_o)
-    return float(d.max()), float(d.mean())
-
-
-# tolerance of the GPU path against the oracle (bf16 inputs, bf16 output):
-# the stated bar for O
-MAX_ABS = 1e-2
-MEAN_ABS = 1e-3
-# lse (natural log): the row sum adds softmax weights rounded to bf16, each
-# within a relative 2^-9 of its exact value, so ln(l) moves by at most 2^-9;
-# fp32 scores add well under 1e-4 at these magnitudes
-LSE_ABS = 2.0 ** -9 + 1e-4
