@@ -17,19 +17,20 @@
 //     p iff j <= p (only on steps that reach past the wave's smallest
 //     position; a wave stops computing after the step holding its largest
 //     position, while it keeps copying its share and meeting the barriers);
-//   - online softmax in fp32 in the exp2 domain: the row max is taken on the
-//     raw scores, scale * log2(e) enters one FMA per score; the reference max
-//     only moves (and O is only rescaled) when a row's max grows by more than
-//     2^8; the row sum adds the bf16-rounded weights with v_dot2 against (1, 1);
+//   - online softmax in fp32 in the exp2 domain: scale * log2(e) enters one
+//     FMA per score against a reference max that only moves (and O is only
+//     rescaled) when a row's max grows by more than 2^8.  The row max itself
+//     is only taken when a step's weights may have outgrown the reference
+//     (see settle); the row sum adds the bf16-rounded weights with v_dot2
+//     against (1, 1);
 //   - O^T += V^T P^T on the same MFMA, P packed to bf16 straight from the
 //     score registers.  The A-operand row order of K is permuted (bits 2 and 3
 //     of the row index swapped) so that the 8 scores a lane feeds to one PV
 //     step are 8 consecutive keys, a single 16-byte LDS read of V^T.
 // Steps whose successor needs no mask run software-pipelined in pairs: the
-// QK MFMAs of step j+1 are interleaved with the exponentials of step j, and
-// the PV MFMAs of step j with the row max of step j+1, so that every MFMA is
-// followed by independent vector work.  The diagonal steps and the last one
-// run the same operations without overlap.
+// QK MFMAs of step j+1 are interleaved with the exponentials of step j, so
+// that each of them is followed by independent vector work.  The diagonal
+// steps and the last one run the same operations without overlap.
 // msa_merge: combines the per-split partials of a split tile by log-sum-exp.
 #include <hip/hip_runtime.h>
 
@@ -87,19 +88,20 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// 16 bytes per lane from global memory straight into LDS at
-// lds + 16 * lane (a wave copies 1 KB; M0 holds the wave's LDS base);
-// completion is tracked by vmcnt.  Issued as inline assembly: when the
-// compiler sees these copies it treats the LDS counter as unordered and
-// waits for every outstanding LDS read (lgkmcnt(0)) before each MFMA, which
-// cancels the operand read-ahead.  The kernel itself waits for the copies
-// (wait_dma) before the barrier that publishes them; the compiler's own
-// vmcnt waits stay correct because vector loads complete in issue order,
-// so extra loads it does not count only make those waits stricter.  The
-// s_nop covers the M0-write-to-LDS-DMA hazard.
-__device__ __forceinline__ void dma16(const void* g, void* lds) {
+// 16 bytes per lane from global memory (wave-uniform base + per-lane 32-bit
+// byte offset) straight into LDS at lds + 16 * lane (a wave copies 1 KB; M0
+// holds the wave's LDS base); completion is tracked by vmcnt.  The base goes
+// in scalar registers, so the copy needs no vector address arithmetic.
+// Issued as inline assembly: when the compiler sees these copies it treats
+// the LDS counter as unordered and waits for every outstanding LDS read
+// (lgkmcnt(0)) before each MFMA, which cancels the operand read-ahead.  The
+// kernel itself waits for the copies (wait_dma) before the barrier that
+// publishes them; the compiler's own vmcnt waits stay correct because vector
+// loads complete in issue order, so extra loads it does not count only make
+// those waits stricter.  The s_nop covers the M0-write-to-LDS-DMA hazard.
+__device__ __forceinline__ void dma16(const void* base, uint32_t off, void* lds) {
   const uint32_t l = (uint32_t)(uintptr_t)(lds_void_t*)lds;
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(l) : "memory");
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(l) : "memory");
 }
 // wait until at most n copies issued by this wave are outstanding
 template <int n>
@@ -126,6 +128,8 @@ __device__ __forceinline__ int32_t sload_i32(const int32_t* a) {
 // when a row's max grows by more than this (log2 units), so the unnormalised
 // weights stay <= 2^8
 constexpr float kRescaleLog2 = 8.0f;
+// a lane's step sum of weights at which the row max is taken (see settle)
+constexpr float kSettleSum = 128.0f;
 
 template <int D, int W>
 __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
@@ -231,12 +235,12 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
           const char* kg = kbase + ids[k] * ksb;
           char* kd = kbuf(sk) + bi * T::kPage;
 #pragma unroll
-          for (int q = 0; q < T::kDmaPerPage; ++q) dma16(kg + kgo[q], kd + q * 1024);
+          for (int q = 0; q < T::kDmaPerPage; ++q) dma16(kg, kgo[q], kd + q * 1024);
         } else {
           const char* vg = vbase + ids[k] * vsb;
           char* vd = vbuf(sv) + bi * T::kPage;
 #pragma unroll
-          for (int q = 0; q < T::kDmaPerPage; ++q) dma16(vg + q * vgq + vgo0, vd + q * 1024);
+          for (int q = 0; q < T::kDmaPerPage; ++q) dma16(vg + q * vgq, vgo0, vd + q * 1024);
         }
       } else if (zero[k]) {
 #pragma unroll
@@ -262,19 +266,26 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   constexpr int kAhead = 3;                           // operand reads issued ahead of their MFMA
 
   // K operand of QK MFMA i of step s (register i of a lane: key row kt*32 + krow_m)
-  auto kread = [&](int s, int i) -> bf16x8 {
+  auto kread_at = [&](const char* kb, int i) -> bf16x8 {
     const int kk = i >> 1, kt = i & 1;
     const int row = kt * 32 + krow_m;
-    return *reinterpret_cast<const bf16x8*>(kbuf(s) + row * (2 * D) + (((kk * 2 + hl) ^ kswz(row)) * 16));
+    return *reinterpret_cast<const bf16x8*>(kb + row * (2 * D) + (((kk * 2 + hl) ^ kswz(row)) * 16));
   };
-  auto vread = [&](int s, int i) -> bf16x8 {
+  auto vread_at = [&](const char* vb, int i) -> bf16x8 {
     const int ks = i / (D / 32), dt = i % (D / 32);
-    return *reinterpret_cast<const bf16x8*>(vbuf(s) + ks * T::kPage + (dt * 32 + ln) * 32 + vsw);
+    return *reinterpret_cast<const bf16x8*>(vb + ks * T::kPage + (dt * 32 + ln) * 32 + vsw);
+  };
+  auto kread = [&](int s, int i) { return kread_at(kbuf(s), i); };
+  auto vread = [&](int s, int i) { return vread_at(vbuf(s), i); };
+  // the same with the ring stage known at compile time: its offset then
+  // folds into the reads' immediate offsets
+  auto kread_c = [&](auto st, int i) { return kread_at(smem + decltype(st)::value * T::kBytesK, i); };
+  auto vread_c = [&](auto st, int i) {
+    return vread_at(smem + 2 * T::kBytesK + decltype(st)::value * T::kBytesV, i);
   };
   // score e (0..31) of a lane sits in tile e/16, register e%16
 
   f32x16 sbuf[2][2];
-  float mx_next = -__builtin_inff();
 
   // QK of step s into sbuf[b] (no interleaving; prologue only)
   auto qk_plain = [&](int b, int s) {
@@ -290,56 +301,78 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
       }
     }
   };
-  // mask + max of step s held in sbuf[b] (plain, prologue only)
-  auto max_plain = [&](int b, int s, auto masked) {
-    constexpr bool kM = decltype(masked)::value;
+  // causal mask of step s applied to the scores in sbuf[b]
+  auto mask_plain = [&](int b, int s) {
     const int lim = pos - (w.kv_lo + s * kKvStep) - hl * 8;
-    float mx = -__builtin_inff();
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
-      float x = sbuf[b][e >> 4][e & 15];
-      if constexpr (kM) x = ((e >> 4) * 32 + ((e & 15) >> 3) * 16 + (e & 7)) <= lim ? x : -__builtin_inff();
-      sbuf[b][e >> 4][e & 15] = x;
-      mx = fmaxf(mx, x);
+      const float x = sbuf[b][e >> 4][e & 15];
+      sbuf[b][e >> 4][e & 15] = ((e >> 4) * 32 + ((e & 15) >> 3) * 16 + (e & 7)) <= lim ? x : -__builtin_inff();
     }
-    mx_next = mx;
   };
-  // move the reference max of the step whose raw max is mx_next (rare)
-  auto rescale = [&]() {
-    const float m_blk = pair_max(mx_next) * c;
-    const bool grow = m_blk > m_ref + kRescaleLog2;
-    if (__any(grow)) {  // wave-uniform
-      const float alpha = grow ? __builtin_amdgcn_exp2f(m_ref - m_blk) : 1.0f;
-      m_ref = grow ? m_blk : m_ref;
-      l_run *= alpha;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  // weights of the scores in sbuf[b] against the reference max, packed to
+  // bf16; ls gets their sum (the row sum adds the same bf16-rounded weights
+  // that enter the PV product, so the normalised weights sum to one exactly)
+  auto weights_plain = [&](int b, uint32_t (&pk)[16], float& ls) {
+    const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
+    ls = 0.0f;
 #pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+    for (int e = 0; e < 32; e += 2) {
+      pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][e >> 4][e & 15], c, nm)),
+                               __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][(e + 1) >> 4][(e + 1) & 15], c, nm)));
+      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
+    }
+  };
+  // The row max is only taken when the weights of a step may have outgrown
+  // the reference: a lane's step sum reached 2^7, or the row has no
+  // reference yet.  A row whose max exceeds the reference by more than 2^8
+  // (in log2 units) holds a weight >= 2^8, so its lane's sum passes 2^7:
+  // the reference moves exactly as if the max were taken every step.  The
+  // weights are then recomputed against the new reference.
+  auto settle = [&](int b, uint32_t (&pk)[16], float& ls) {
+    if (__any(!(ls < kSettleSum) || m_ref == -__builtin_inff())) {  // wave-uniform
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int e = 0; e < 32; ++e) mx = fmaxf(mx, sbuf[b][e >> 4][e & 15]);
+      const float m_blk = pair_max(mx) * c;
+      const bool grow = m_blk > m_ref + kRescaleLog2;
+      if (__any(grow)) {
+        const float alpha = grow ? __builtin_amdgcn_exp2f(m_ref - m_blk) : 1.0f;
+        m_ref = grow ? m_blk : m_ref;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+        weights_plain(b, pk, ls);
+      }
     }
   };
 
-  // One step j, scores of step j in sbuf[B] (masked, max applied):
-  //   block 1: QK of step j+1 into sbuf[1-B], interleaved with the weights of step j
-  //   block 2: PV of step j, interleaved with mask + max of step j+1
-  // The source order is fixed with scheduling fences so that every MFMA is
-  // followed by independent vector work of the other half of the pipeline.
+  // One step j, scores of step j in sbuf[B] (masked):
+  //   block 1: QK of step j+1 into sbuf[1-B], interleaved with the weights of
+  //            step j; then settle the weights of step j (rarely does work)
+  //   block 2: PV of step j (on diagonal steps interleaved with the mask of
+  //            step j+1)
+  // The source order is fixed with scheduling fences.  j has the parity of
+  // B (the paired loop starts at step 0), so step j+1's K sits in ring stage
+  // 1-B and step j's V in stage B.
   auto fused = [&](auto bsel, auto mask_next, auto has_next, int j) {
     constexpr int B = decltype(bsel)::value, NB = 1 - B;
     constexpr bool kMaskNext = decltype(mask_next)::value;
     constexpr bool kNext = decltype(has_next)::value;
     const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
     uint32_t pk[16];
     float ls = 0.0f;
     // block 1
     bf16x8 ka[kQk];
     if constexpr (kNext) {
 #pragma unroll
-      for (int a = 0; a < kAhead; ++a) ka[a] = kread(j + 1, a);
+      for (int a = 0; a < kAhead; ++a) ka[a] = kread_c(std::integral_constant<int, NB>{}, a);
     }
 #pragma unroll
     for (int i = 0; i < kQk; ++i) {
       if constexpr (kNext) {
-        if (i + kAhead < kQk) ka[i + kAhead] = kread(j + 1, i + kAhead);
+        if (i + kAhead < kQk) ka[i + kAhead] = kread_c(std::integral_constant<int, NB>{}, i + kAhead);
         const int kk = i >> 1, kt = i & 1;
         if (kk == 0) {
           const f32x16 zero = {};
@@ -353,41 +386,34 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
         const int e = i * kElPerQk + u;
         pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][e >> 4][e & 15], c, nm)),
                                  __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][(e + 1) >> 4][(e + 1) & 15], c, nm)));
-        // the row sum adds the same bf16-rounded weights that enter the PV
-        // product, so the normalised weights sum to one exactly
         ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    settle(B, pk, ls);
     l_run += ls;
     // block 2
     const int lim = pos - (w.kv_lo + (j + 1) * kKvStep) - hl * 8;
-    float mx = -__builtin_inff();
     bf16x8 va[kPv];
 #pragma unroll
-    for (int a = 0; a < kAhead; ++a) va[a] = vread(j, a);
+    for (int a = 0; a < kAhead; ++a) va[a] = vread_c(std::integral_constant<int, B>{}, a);
 #pragma unroll
     for (int i = 0; i < kPv; ++i) {
-      if (i + kAhead < kPv) va[i + kAhead] = vread(j, i + kAhead);
+      if (i + kAhead < kPv) va[i + kAhead] = vread_c(std::integral_constant<int, B>{}, i + kAhead);
       const int ks = i / (D / 32), dt = i % (D / 32);
       // P sub-step ks = keys 16*ks + hl*8 .. +8 = packed weights 4*ks .. 4*ks+3
       const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
       oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pb, oacc[dt], 0, 0, 0);
-      if constexpr (kNext) {
+      if constexpr (kNext && kMaskNext) {
 #pragma unroll
         for (int u = 0; u < kElPerPv; ++u) {
           const int e = i * kElPerPv + u;
-          float x = sbuf[NB][e >> 4][e & 15];
-          if constexpr (kMaskNext) {
-            x = ((e >> 4) * 32 + ((e & 15) >> 3) * 16 + (e & 7)) <= lim ? x : -__builtin_inff();
-            sbuf[NB][e >> 4][e & 15] = x;
-          }
-          mx = fmaxf(mx, x);
+          const float x = sbuf[NB][e >> 4][e & 15];
+          sbuf[NB][e >> 4][e & 15] = ((e >> 4) * 32 + ((e & 15) >> 3) * 16 + (e & 7)) <= lim ? x : -__builtin_inff();
         }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    mx_next = mx;
   };
 
   // Step s's K sits in K buffer s % 2 and its V in V buffer s % 2; in
@@ -405,8 +431,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   lds_barrier();
   if (nw > 0) {
     qk_plain(0, 0);
-    if (need_mask(0)) max_plain(0, 0, std::true_type{}); else max_plain(0, 0, std::false_type{});
-    rescale();
+    if (need_mask(0)) mask_plain(0, 0);
   }
   lds_barrier();  // every wave is done with K_0 before K_2 replaces it
 
@@ -417,8 +442,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   // ones and the last) one at a time, copying the next scores back to
   // sbuf[0].  Waves may split their steps differently between the loops;
   // every step still ends with exactly one barrier.
-  auto tail = [&](int j) {
-    if (j + 1 < nw) rescale();
+  auto tail = [&]() {
     wait_dma<0>();
     lds_barrier();
   };
@@ -426,25 +450,19 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   for (; j + 2 < nw && !need_mask(j + 2); j += 2) {
     issue(j + 2, j + 1);
     fused(std::integral_constant<int, 0>{}, std::false_type{}, std::true_type{}, j);
-    tail(j);
+    tail();
     issue(j + 3, j + 2);
     fused(std::integral_constant<int, 1>{}, std::false_type{}, std::true_type{}, j + 1);
-    tail(j + 1);
+    tail();
   }
   // Remaining steps (the diagonal ones and the last) run without overlap:
-  // weights of step j, PV of step j, then QK + mask + max of step j+1 into
-  // the same score registers.  Same copy schedule as the pipelined loop.
+  // weights of step j, PV of step j, then QK + mask of step j+1 into the
+  // same score registers.  Same copy schedule as the pipelined loop.
   auto plain = [&](int jj) {
-    const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
     uint32_t pk[16];
-    float ls = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 32; e += 2) {
-      pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[0][e >> 4][e & 15], c, nm)),
-                               __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[0][(e + 1) >> 4][(e + 1) & 15], c, nm)));
-      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
-    }
+    float ls;
+    weights_plain(0, pk, ls);
+    settle(0, pk, ls);
     l_run += ls;
 #pragma unroll
     for (int i = 0; i < kPv; ++i) {
@@ -454,13 +472,13 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
     }
     if (jj + 1 < nw) {
       qk_plain(0, jj + 1);
-      if (need_mask(jj + 1)) max_plain(0, jj + 1, std::true_type{}); else max_plain(0, jj + 1, std::false_type{});
+      if (need_mask(jj + 1)) mask_plain(0, jj + 1);
     }
   };
   for (; j < n; ++j) {
     issue(j + 2, j + 1);
     if (j < nw) plain(j);
-    tail(j);
+    tail();
   }
 
   // epilogue: lane (hl, ln) holds row r, channels dt*32 + (i/4)*8 + hl*4 + i%4
