@@ -102,15 +102,21 @@ typedef struct msa_plan_opts {
 #define MSA_PLAN_HOST_ONLY 1
 /* Disable the cost-based automatic key splitting (forced splits still apply). */
 #define MSA_PLAN_NO_AUTO_SPLIT 2
-/* Force the tile width (query rows x heads per workgroup).  Without either
- * flag the planner takes 256-row tiles (one workgroup per CU; each K/V step
- * is loaded once for twice the rows) when the plan has many tiles and a
- * long run of key steps per workgroup slot, and 128-row tiles (two
- * workgroups per CU: one's start-up and tail overlap the other's work, more
- * concurrent key streams) for small, short and decode-heavy plans.  The two
- * flags are exclusive. */
+/* Force the tile width (query rows x heads per workgroup).  Without a flag
+ * the planner takes:
+ *   - 32-row tiles when no 128-row tile would hold more than 32 rows
+ *     (decode-like plans: the four waves of a workgroup split the tile's
+ *     keys and read K and V straight into registers, two workgroups per CU);
+ *   - 256-row tiles (one workgroup per CU; each K/V step is loaded once for
+ *     twice the rows) when the plan has many tiles and a long run of key
+ *     steps per workgroup slot;
+ *   - else 128-row tiles (two workgroups per CU: one's start-up and tail
+ *     overlap the other's work).
+ * The flags are exclusive.  32-row tiles need Hq / Hkv <= 32, 128-row tiles
+ * Hq / Hkv <= 128 (else MSA_ERR_UNSUPPORTED). */
 #define MSA_PLAN_TILE_ROWS_128 4
 #define MSA_PLAN_TILE_ROWS_256 8
+#define MSA_PLAN_TILE_ROWS_32 16
 
 /* Figures describing a plan. */
 typedef struct msa_plan_info_t {
@@ -124,7 +130,7 @@ typedef struct msa_plan_info_t {
   double tile_flops;        /* flops the tiles issue (waves holding rows), incl. masked waste */
   double planned_bytes;     /* Q + O + K/V bytes the executed tiles request */
   double min_bytes;         /* Q + O + K/V of visible keys once per (seq, kv head) */
-  int64_t tile_rows;        /* rows per tile of this plan: 128 or 256 */
+  int64_t tile_rows;        /* rows per tile of this plan: 32, 128 or 256 */
 } msa_plan_info_t;
 
 /*
@@ -147,7 +153,8 @@ typedef struct msa_plan_info_t {
  *
  * Returns MSA_ERR_INVALID_ARG for malformed descriptors or shapes,
  * MSA_ERR_UNSUPPORTED for head_dim not in {64, 128}, block_size != 16,
- * Hq / Hkv > 256, or Hq / Hkv > 128 with MSA_PLAN_TILE_ROWS_128;
+ * Hq / Hkv > 256, Hq / Hkv > 128 with MSA_PLAN_TILE_ROWS_128, or Hq / Hkv > 32
+ * with MSA_PLAN_TILE_ROWS_32;
  * MSA_ERR_OUT_OF_MEMORY; MSA_ERR_DEVICE.
  */
 msa_status msa_plan(const msa_shape *shape, const int32_t *seq_kv_len, const int32_t *seg_indptr,

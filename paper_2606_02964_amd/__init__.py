@@ -42,6 +42,7 @@ MSA_PLAN_HOST_ONLY = 1
 MSA_PLAN_NO_AUTO_SPLIT = 2
 MSA_PLAN_TILE_ROWS_128 = 4
 MSA_PLAN_TILE_ROWS_256 = 8
+MSA_PLAN_TILE_ROWS_32 = 16
 
 _i32, _i64, _f32, _f64, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 

@@ -516,6 +516,249 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   }
 }
 
+// msa_decode: tiles of up to 32 rows (decode-like plans).  Every wave of the
+// 4-wave workgroup holds the same 32 rows; wave w takes the 32-key
+// half-steps w, w + 4, w + 8, ... of the item's key range and reads their K
+// and V straight from the cache into MFMA operand registers.  A tile this
+// small gains nothing from sharing K/V between waves through LDS, and
+// registers hold more bytes in flight: each wave keeps the K of its next
+// half-step and the V of its current one loading while it computes.  The
+// four partial softmax states (max, sum, O) are merged through LDS at the
+// end.  Arithmetic per half-step is that of the main kernel: S^T = K Q^T
+// with K's rows permuted (bits 2 and 3 swapped), the lazy reference max and
+// bf16 weights whose row sum uses the same rounded values.
+template <int D>
+__global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
+  constexpr int kWaves = 4, kHalf = 32;
+  constexpr int kOPad = D + 4;  // LDS row stride of the partial O (bank spread)
+  __shared__ __attribute__((aligned(16))) float mo[kWaves][32][kOPad];
+  __shared__ float mm[kWaves][32], ml[kWaves][32];
+
+  const WorkItem w = p.work[blockIdx.x];
+  if (w.nrows == 0) return;  // padding item (uniform over the workgroup)
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
+  const int G = p.group;
+  const int t = ln / G, hh = ln - t * G;  // tile row ln <-> token t, head hh of the group
+  const bool valid = t < w.nrows;
+  const int tok = w.row0 + t;
+  const int head = w.kv_head * G + hh;
+  const int pos = valid ? p.row_pos[tok] : -1;
+  int pmin = valid ? pos : INT_MAX, pmax = pos;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    pmin = min(pmin, __shfl_xor(pmin, off));
+    pmax = max(pmax, __shfl_xor(pmax, off));
+  }
+  pmin = __builtin_amdgcn_readfirstlane(pmin);
+  pmax = __builtin_amdgcn_readfirstlane(pmax);
+
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t* qrow = p.q + (int64_t)tok * p.q_st + (int64_t)head * p.q_sh + hl * 8;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      if (valid) {
+        qf[kk] = *reinterpret_cast<const bf16x8*>(qrow + kk * 16);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) qf[kk][j] = (__bf16)0.0f;
+      }
+    }
+  }
+
+  const char* kbase = reinterpret_cast<const char*>(p.k + (int64_t)w.kv_head * p.k_sh);
+  const char* vbase = reinterpret_cast<const char*>(p.v + (int64_t)w.kv_head * p.v_sh);
+  const int32_t* bt = p.block_table + (int64_t)w.seq * p.max_blocks;
+  const int64_t ksb = p.k_sb * 2, vsb = p.v_sb * 2;  // bytes per block
+  const int krow = swap_bits23(ln);                   // key (0..31 in the half-step) of MFMA row ln
+  // per-lane byte offsets inside a block: K row krow % 16 at channel hl*8
+  // (+ kk*16 per fragment); V^T row (channel) ln at keys hl*8 (+ dt*32 rows)
+  const uint32_t koff = (uint32_t)((krow & 15) * p.k_st + hl * 8) * 2u;
+  const uint32_t voff = (uint32_t)(ln * p.v_sd + hl * 8) * 2u;
+  const uint32_t vdt = (uint32_t)(32 * p.v_sd) * 2u;
+
+  const int nh = (w.kv_hi - w.kv_lo + kHalf - 1) / kHalf;
+  // half-steps holding keys up to the tile's largest position
+  const int nhw = pmax >= w.kv_lo ? min(nh, (pmax - w.kv_lo) / kHalf + 1) : 0;
+  // The two blocks of half-step h.  The second one is only read when it
+  // holds a key of the range; otherwise the first one stands in (its keys
+  // are then past every row's position, hence masked).  The ids of this
+  // wave's first 64 half-steps (h = wave + 4i) are loaded once, lane i
+  // holding those of half-step i, so that no half-step waits for a table
+  // read; later half-steps read the table directly.
+  auto table_blocks = [&](int h, int32_t& id0, int32_t& id1) {
+    const int k0 = w.kv_lo + h * kHalf;
+    id0 = bt[k0 >> 4];
+    id1 = k0 + kBlockSize < w.kv_hi ? bt[(k0 >> 4) + 1] : id0;
+  };
+  int32_t idv0 = 0, idv1 = 0;
+  if (wave + kWaves * lane < nhw) table_blocks(wave + kWaves * lane, idv0, idv1);
+  auto blocks = [&](int h, int64_t& id0, int64_t& id1) __attribute__((always_inline)) {
+    const int i = (h - wave) / kWaves;  // wave-uniform
+    if (i < 64) {
+      id0 = __builtin_amdgcn_readlane(idv0, i);
+      id1 = __builtin_amdgcn_readlane(idv1, i);
+    } else {
+      int32_t a, b;
+      table_blocks(h, a, b);
+      id0 = a;
+      id1 = b;
+    }
+  };
+  constexpr int kQk = D / 16;       // QK MFMAs per half-step
+  constexpr int kPv = 2 * (D / 32); // PV MFMAs per half-step, ordered (ks, dt)
+  bf16x8 ka[2][kQk], va[kPv];
+  auto load_k = [&](auto bsel, int h) __attribute__((always_inline)) {
+    constexpr int b = decltype(bsel)::value;
+    int64_t id0, id1;
+    blocks(h, id0, id1);
+    const char* kb = kbase + (krow >= 16 ? id1 : id0) * ksb + koff;
+#pragma unroll
+    for (int kk = 0; kk < kQk; ++kk) ka[b][kk] = *reinterpret_cast<const bf16x8*>(kb + kk * 32);
+  };
+  auto load_v = [&](int h) __attribute__((always_inline)) {
+    int64_t id0, id1;
+    blocks(h, id0, id1);
+#pragma unroll
+    for (int i = 0; i < kPv; ++i) {
+      const int ks = i / (D / 32), dt = i % (D / 32);
+      va[i] = *reinterpret_cast<const bf16x8*>(vbase + (ks ? id1 : id0) * vsb + voff + dt * vdt);
+    }
+  };
+
+  const float c = p.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float m_ref = -__builtin_inff(), l_run = 0.0f;
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.0f;
+
+  // one half-step h of this wave, its K in buffer b
+  auto half = [&](auto bsel, int h) __attribute__((always_inline)) {
+    constexpr int b = decltype(bsel)::value;
+    load_v(h);
+    if (h + kWaves < nhw) load_k(std::integral_constant<int, 1 - b>{}, h + kWaves);
+    f32x16 sc = {};
+#pragma unroll
+    for (int kk = 0; kk < kQk; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[b][kk], qf[kk], sc, 0, 0, 0);
+    // score e (0..15) of a lane is key (e / 8) * 16 + hl * 8 + e % 8 of the half-step
+    const int k0 = w.kv_lo + h * kHalf;
+    if (k0 + kHalf - 1 > pmin) {
+      const int lim = pos - k0 - hl * 8;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[e] = ((e >> 3) * 16 + (e & 7)) <= lim ? sc[e] : -__builtin_inff();
+    }
+    uint32_t pk[8];
+    float ls;
+    auto weights = [&]() {
+      const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
+      ls = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) {
+        pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm)),
+                                 __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e + 1], c, nm)));
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
+      }
+    };
+    weights();
+    // the lazy reference max of the main kernel
+    if (__any(!(ls < kSettleSum) || m_ref == -__builtin_inff())) {
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[e]);
+      const float m_blk = pair_max(mx) * c;
+      const bool grow = m_blk > m_ref + kRescaleLog2;
+      if (__any(grow)) {
+        const float alpha = grow ? __builtin_amdgcn_exp2f(m_ref - m_blk) : 1.0f;
+        m_ref = grow ? m_blk : m_ref;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+        weights();
+      }
+    }
+    l_run += ls;
+#pragma unroll
+    for (int i = 0; i < kPv; ++i) {
+      const int ks = i / (D / 32), dt = i % (D / 32);
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
+      oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pb, oacc[dt], 0, 0, 0);
+    }
+  };
+  if (wave < nhw) load_k(std::integral_constant<int, 0>{}, wave);
+  for (int h = wave; h < nhw; h += 2 * kWaves) {
+    half(std::integral_constant<int, 0>{}, h);
+    if (h + kWaves < nhw) half(std::integral_constant<int, 1>{}, h + kWaves);
+  }
+
+  // merge the waves' partial states: lane (hl, ln) holds row ln, channels
+  // dt*32 + (i/4)*8 + hl*4 + i%4
+  const float l_tot = pair_sum(l_run);
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      f32x4 v;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = oacc[dt][g4 * 4 + q];
+      *reinterpret_cast<f32x4*>(&mo[wave][ln][dt * 32 + g4 * 8 + hl * 4]) = v;
+    }
+  if (hl == 0) {
+    mm[wave][ln] = m_ref;
+    ml[wave][ln] = l_tot;
+  }
+  __syncthreads();
+  constexpr int kCh = D / 8;  // channels per thread: 32 rows x 8 threads
+  const int row = tid >> 3, c0 = (tid & 7) * kCh;
+  const int rt = row / G, rh = row - rt * G;
+  if (rt >= w.nrows) return;
+  float M = -__builtin_inff();
+#pragma unroll
+  for (int u = 0; u < kWaves; ++u) M = fmaxf(M, mm[u][row]);
+  float L = 0.0f, acc[kCh];
+#pragma unroll
+  for (int q = 0; q < kCh; ++q) acc[q] = 0.0f;
+#pragma unroll
+  for (int u = 0; u < kWaves; ++u) {
+    const float f = mm[u][row] == -__builtin_inff() ? 0.0f : __builtin_amdgcn_exp2f(mm[u][row] - M);
+    L += f * ml[u][row];
+#pragma unroll
+    for (int q = 0; q < kCh; q += 4) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(&mo[u][row][c0 + q]);
+#pragma unroll
+      for (int z = 0; z < 4; ++z) acc[q + z] += f * v[z];
+    }
+  }
+  const int otok = w.row0 + rt, ohead = w.kv_head * G + rh;
+  if (w.out_slot < 0) {
+    const float inv = 1.0f / L;
+    uint16_t* orow = p.o + (int64_t)otok * p.o_st + (int64_t)ohead * p.o_sh + c0;
+#pragma unroll
+    for (int q = 0; q < kCh; q += 4)
+      *reinterpret_cast<uint2*>(orow + q) = make_uint2(pack_bf16x2(acc[q] * inv, acc[q + 1] * inv),
+                                                       pack_bf16x2(acc[q + 2] * inv, acc[q + 3] * inv));
+    if (p.lse && c0 == 0) p.lse[(int64_t)otok * p.num_q_heads + ohead] = (M + __log2f(L)) * kLn2;
+  } else {
+    constexpr int kR = 32;  // rows of a workspace slot of this tile width
+    float* slot = p.ws + (int64_t)w.out_slot * kR * (D + 1);
+    const bool empty = !(L > 0.0f);  // no visible key in this split
+    const float inv = empty ? 0.0f : 1.0f / L;
+#pragma unroll
+    for (int q = 0; q < kCh; q += 4) {
+      f32x4 v;
+#pragma unroll
+      for (int z = 0; z < 4; ++z) v[z] = acc[q + z] * inv;
+      *reinterpret_cast<f32x4*>(slot + row * D + c0 + q) = v;
+    }
+    if (c0 == 0) slot[kR * D + row] = empty ? -__builtin_inff() : (M + __log2f(L)) * kLn2;
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void msa_merge_kernel(MergeParams p) {
   constexpr int kThreadsPerRow = D / 4;
@@ -564,6 +807,10 @@ int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_work, 
     hipLaunchKernelGGL((msa_attn_kernel<64, 4>), dim3(num_work), dim3(256), 0, s, p);
   else if (head_dim == 64 && tile_rows == kTileRowsWide)
     hipLaunchKernelGGL((msa_attn_kernel<64, 8>), dim3(num_work), dim3(512), 0, s, p);
+  else if (head_dim == 128 && tile_rows == kTileRowsDecode)
+    hipLaunchKernelGGL(msa_decode_kernel<128>, dim3(num_work), dim3(256), 0, s, p);
+  else if (head_dim == 64 && tile_rows == kTileRowsDecode)
+    hipLaunchKernelGGL(msa_decode_kernel<64>, dim3(num_work), dim3(256), 0, s, p);
   else
     return (int)hipErrorInvalidValue;
   return (int)hipGetLastError();

@@ -13,12 +13,14 @@
 
 namespace msa {
 
-// Two tile widths: 128 rows (4 waves x 32 rows, two workgroups per CU) for
-// small or decode-heavy plans, 256 rows (8 waves, one workgroup per CU) for
-// plans with many tiles: a wider tile loads each K/V step once for twice the
-// rows.
+// Tile widths: 128 rows (4 waves x 32 rows, two workgroups per CU) for
+// small plans, 256 rows (8 waves, one workgroup per CU) for plans with many
+// tiles (a wider tile loads each K/V step once for twice the rows), and 32
+// rows for decode-like plans (every tile holds at most 32 rows; the four
+// waves split the tile's keys and read K/V straight into registers).
 constexpr int kTileRowsNarrow = 128;
 constexpr int kTileRowsWide = 256;
+constexpr int kTileRowsDecode = 32;
 constexpr int kKvStep = 64;      // keys per main-loop iteration (4 blocks of 16)
 constexpr int kBlockSize = 16;
 

@@ -14,10 +14,14 @@
 //      128-row tiling has many tiles and a long run of key steps per
 //      workgroup slot, else 128 (two workgroups per CU: one's start-up and
 //      tail overlap the other's work, and decode-heavy plans keep more key
-//      streams in flight);
+//      streams in flight); it is 32 when no 128-row tile would hold more
+//      than 32 rows (decode-like plans: the four waves of a workgroup then
+//      split the tile's keys);
 //   3. units: tile x KV head, keys [0, max position in tile + 1);
-//   4. key splits: units much longer than the average share of a workgroup
-//      slot are cut into 64-aligned key ranges, merged later by log-sum-exp;
+//   4. key splits: units longer than a third of a workgroup slot's share of
+//      the work are cut into 64-aligned key ranges, merged later by
+//      log-sum-exp; with 32-row tiles the cut length is the shortest whose
+//      pieces all fit one round of the workgroup slots;
 //   5. order: (sequence, KV head) groups are spread over the 8 XCDs (blockIdx
 //      i runs on XCD i % 8) so tiles sharing K/V share one XCD's L2.  Inside
 //      each XCD, groups start in decreasing order of their longest piece and
@@ -67,10 +71,14 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   for (int i = 0; i < 5; ++i)
     if (o.reserved[i] != 0) return fail(err, MSA_ERR_INVALID_ARG, "opts.reserved must be zero");
   if (o.flags & ~(MSA_PLAN_HOST_ONLY | MSA_PLAN_NO_AUTO_SPLIT | MSA_PLAN_TILE_ROWS_128 |
-                  MSA_PLAN_TILE_ROWS_256))
+                  MSA_PLAN_TILE_ROWS_256 | MSA_PLAN_TILE_ROWS_32))
     return fail(err, MSA_ERR_INVALID_ARG, "unknown opts.flags bits");
-  if ((o.flags & MSA_PLAN_TILE_ROWS_128) && (o.flags & MSA_PLAN_TILE_ROWS_256))
-    return fail(err, MSA_ERR_INVALID_ARG, "MSA_PLAN_TILE_ROWS_128 and _256 are exclusive");
+  {
+    const int forced = !!(o.flags & MSA_PLAN_TILE_ROWS_128) + !!(o.flags & MSA_PLAN_TILE_ROWS_256) +
+                       !!(o.flags & MSA_PLAN_TILE_ROWS_32);
+    if (forced > 1)
+      return fail(err, MSA_ERR_INVALID_ARG, "MSA_PLAN_TILE_ROWS_32, _128 and _256 are exclusive");
+  }
 
   if (s.num_seqs < 0) return fail(err, MSA_ERR_INVALID_ARG, "num_seqs < 0");
   if (s.num_q_heads < 1 || s.num_kv_heads < 1)
@@ -81,6 +89,8 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   if (G > kTileRowsWide) return fail(err, MSA_ERR_UNSUPPORTED, "num_q_heads / num_kv_heads > 256");
   if (G > kTileRowsNarrow && (o.flags & MSA_PLAN_TILE_ROWS_128))
     return fail(err, MSA_ERR_UNSUPPORTED, "128-row tiles need num_q_heads / num_kv_heads <= 128");
+  if (G > kTileRowsDecode && (o.flags & MSA_PLAN_TILE_ROWS_32))
+    return fail(err, MSA_ERR_UNSUPPORTED, "32-row tiles need num_q_heads / num_kv_heads <= 32");
   if (s.head_dim <= 0) return fail(err, MSA_ERR_INVALID_ARG, "head_dim <= 0");
   if (s.head_dim != 64 && s.head_dim != 128)
     return fail(err, MSA_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
@@ -181,22 +191,32 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     return units;
   };
 
-  // tile width: forced by a flag, else wide when the narrow tiling has many
-  // tiles and enough work per workgroup slot (G > 128 needs wide tiles)
+  // tile width: forced by a flag, else 32 rows when no 128-row tile would
+  // hold more than 32 rows (decode-like plans), wide when the narrow tiling
+  // has many tiles and enough work per workgroup slot (G > 128 needs wide
+  // tiles), else narrow
   const int32_t narrow_tokens = G <= kTileRowsNarrow ? kTileRowsNarrow / G : 0;
   std::vector<Unit> narrow_units;
   {
     int32_t rows = kTileRowsNarrow;
     if (o.flags & MSA_PLAN_TILE_ROWS_256) {
       rows = kTileRowsWide;
+    } else if (o.flags & MSA_PLAN_TILE_ROWS_32) {
+      rows = kTileRowsDecode;
     } else if (!(o.flags & MSA_PLAN_TILE_ROWS_128)) {
       if (G > kTileRowsNarrow) {
         rows = kTileRowsWide;
       } else {
         narrow_units = make_units(narrow_tokens);
         double steps = 0;
-        for (const Unit& u : narrow_units) steps += (double)((u.kv_hi + kKvStep - 1) / kKvStep);
-        if ((int64_t)narrow_units.size() >= kWideMinTiles && steps >= kWideMinStepsPerSlot * 2.0 * kCUs)
+        int64_t max_rows = 0;
+        for (const Unit& u : narrow_units) {
+          steps += (double)((u.kv_hi + kKvStep - 1) / kKvStep);
+          max_rows = std::max<int64_t>(max_rows, (int64_t)u.nrows * G);
+        }
+        if (!narrow_units.empty() && max_rows <= kTileRowsDecode)
+          rows = kTileRowsDecode;
+        else if ((int64_t)narrow_units.size() >= kWideMinTiles && steps >= kWideMinStepsPerSlot * 2.0 * kCUs)
           rows = kTileRowsWide;
       }
     }
@@ -239,10 +259,33 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   } else if (!(o.flags & MSA_PLAN_NO_AUTO_SPLIT) && !units.empty()) {
     double total_steps = 0;
     for (const Unit& u : units) total_steps += (double)(steps(u.kv_hi) + 1);
-    // aim at about 3 work items per workgroup slot: a unit longer than this
-    // share of the total is cut into pieces no longer than the share
-    const int64_t share = (int64_t)std::ceil(total_steps / (3.0 * slots_total)) * kKvStep;
-    split_keys = std::max<int64_t>(kMinSplitKeys, share);
+    if (P.tile_rows == kTileRowsDecode) {
+      // 32-row tiles (decode-like, bound by K/V streaming; the four waves of
+      // a workgroup already split an item's keys): all pieces in one round
+      // of the workgroup slots, the longest piece as short as possible, i.e.
+      // the shortest 64-aligned piece length whose piece count fits the
+      // slots (no split if the units alone exceed them)
+      auto pieces_at = [&](int64_t len) {
+        int64_t c = 0;
+        for (const Unit& u : units) c += (u.kv_hi + len - 1) / len;
+        return c;
+      };
+      int64_t longest = 0;
+      for (const Unit& u : units) longest = std::max<int64_t>(longest, u.kv_hi);
+      int64_t lo = kKvStep, hi = (longest + kKvStep - 1) / kKvStep * kKvStep;
+      if ((int64_t)units.size() <= slots_total) {
+        while (lo < hi) {  // smallest length with pieces_at(length) <= slots
+          const int64_t mid = (lo / kKvStep + hi / kKvStep) / 2 * kKvStep;
+          if (pieces_at(mid) <= slots_total) hi = mid; else lo = mid + kKvStep;
+        }
+        split_keys = std::max<int64_t>(kMinSplitKeys, lo);
+      }
+    } else {
+      // aim at about 3 work items per workgroup slot: a unit longer than
+      // this share of the total is cut into pieces no longer than the share
+      const int64_t share = (int64_t)std::ceil(total_steps / (3.0 * slots_total)) * kKvStep;
+      split_keys = std::max<int64_t>(kMinSplitKeys, share);
+    }
   }
   struct Piece {
     int32_t unit, lo, hi, slot;
@@ -373,7 +416,9 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     P.planned_bytes += keys * d * 2.0 * 2.0;
     // waves whose 32 rows are all empty skip every step
     const double rows = (double)((w.nrows * G + 31) / 32 * 32);
-    P.tile_flops += 4.0 * d * rows * (double)steps(w.kv_hi - w.kv_lo) * kKvStep;
+    // 32-row tiles run 32-key half-steps, the others 64-key steps
+    const int64_t gran = P.tile_rows == kTileRowsDecode ? kKvStep / 2 : kKvStep;
+    P.tile_flops += 4.0 * d * rows * (double)((w.kv_hi - w.kv_lo + gran - 1) / gran * gran);
   }
   P.min_bytes = qo_bytes;
   for (int32_t b = 0; b < B; ++b)

@@ -13,7 +13,7 @@ namespace msa {
 struct HostPlan {
   msa_shape shape{};
   int32_t group = 1;        // G = Hq / Hkv
-  int32_t tile_rows = 0;    // rows per tile: kTileRowsNarrow or kTileRowsWide
+  int32_t tile_rows = 0;    // rows per tile: kTileRowsDecode, kTileRowsNarrow or kTileRowsWide
   int32_t tile_tokens = 0;  // query tokens per tile
   int64_t total_q = 0;
   std::vector<int32_t> row_pos;   // [total_q] absolute position of each packed row

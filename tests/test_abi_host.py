@@ -124,7 +124,7 @@ def check_plan(inst, row_pos, work, merge, info, G):
     assert (covered == 1).all(), "every (row, kv head) must be in exactly one tile"
     assert len(merged) == len(merge)
     assert info["total_q"] == total
-    assert info["tile_rows"] in (128, 256)
+    assert info["tile_rows"] in (32, 128, 256)
     assert info["workspace_bytes"] == len(slots_seen) * info["tile_rows"] * (inst.head_dim + 1) * 4
     useful = 4.0 * inst.head_dim * inst.num_q_heads * float((row_pos.astype(np.float64) + 1).sum())
     assert abs(info["useful_flops"] - useful) <= 1e-9 * max(1.0, useful)
@@ -314,9 +314,19 @@ def test_plan_rejects_bad_options(msa):
     with pytest.raises(msa.MsaError) as e:
         host_plan(msa, big_group, flags=msa.MSA_PLAN_TILE_ROWS_128)
     assert e.value.status == msa.MSA_ERR_UNSUPPORTED
+    for both in (msa.MSA_PLAN_TILE_ROWS_128 | msa.MSA_PLAN_TILE_ROWS_256,
+                 msa.MSA_PLAN_TILE_ROWS_32 | msa.MSA_PLAN_TILE_ROWS_128,
+                 msa.MSA_PLAN_TILE_ROWS_32 | msa.MSA_PLAN_TILE_ROWS_256):
+        with pytest.raises(msa.MsaError) as e:
+            host_plan(msa, inst, flags=both)
+        assert e.value.status == msa.MSA_ERR_INVALID_ARG
+    # 32-row tiles hold at most 32 rows: Hq / Hkv <= 32
+    g64 = workloads.make_layout(10, [64], [[(63, 1)]], 64, 1, 64)
     with pytest.raises(msa.MsaError) as e:
-        host_plan(msa, inst, flags=msa.MSA_PLAN_TILE_ROWS_128 | msa.MSA_PLAN_TILE_ROWS_256)
-    assert e.value.status == msa.MSA_ERR_INVALID_ARG
+        host_plan(msa, g64, flags=msa.MSA_PLAN_TILE_ROWS_32)
+    assert e.value.status == msa.MSA_ERR_UNSUPPORTED
+    g32 = workloads.make_layout(10, [64], [[(63, 1)]], 32, 1, 64)
+    assert host_plan(msa, g32, flags=msa.MSA_PLAN_TILE_ROWS_32).info()["tile_rows"] == 32
     # the token cap follows the tile width: 128 / 2 = 64 narrow, 128 wide
     assert host_plan(msa, inst, q_tile_tokens=65, flags=msa.MSA_PLAN_TILE_ROWS_256).info()["tile_rows"] == 256
 
@@ -466,8 +476,9 @@ def _descriptors(kv_lens, segs, hq, hkv, d):
 
 def test_tile_width_choice(msa):
     """Wide (256-row) tiles for plans with many tiles and a long run of key
-    steps per workgroup slot; narrow (128-row) tiles for small, short and
-    decode-only plans; flags force either."""
+    steps per workgroup slot; 32-row tiles when no 128-row tile would hold
+    more than 32 rows (decode-only plans); narrow (128-row) tiles for the
+    other small and short plans; flags force each."""
     for cfg, rows in ((1, 128), (2, 256), (3, 256), (4, 256), (5, 256)):
         assert host_plan(msa, make_layout_only(cfg)).info()["tile_rows"] == rows, cfg
     # many narrow tiles, little work per slot: 8 x 1024-token requests whose
@@ -482,9 +493,42 @@ def test_tile_width_choice(msa):
     keep = [b for b in range(len(lens)) if segs[b] == [(lens[b] - 1, 1)]]  # the decode rows
     decode = _descriptors([lens[b] for b in keep], [segs[b] for b in keep], heads["num_q_heads"],
                           heads["num_kv_heads"], heads["head_dim"])
-    assert host_plan(msa, decode).info()["tile_rows"] == 128
+    assert host_plan(msa, decode).info()["tile_rows"] == 32
     assert host_plan(msa, decode, flags=msa.MSA_PLAN_TILE_ROWS_256).info()["tile_rows"] == 256
+    assert host_plan(msa, decode, flags=msa.MSA_PLAN_TILE_ROWS_128).info()["tile_rows"] == 128
+    # one more decode token per sequence: 2 tokens x 4 heads = 8 rows, still 32-row tiles;
+    # a 16-token chunk in one sequence (64 rows) takes the plan back to 128-row tiles
+    two = _descriptors([lens[b] for b in keep], [[(lens[b] - 2, 2)] for b in keep], heads["num_q_heads"],
+                       heads["num_kv_heads"], heads["head_dim"])
+    assert host_plan(msa, two).info()["tile_rows"] == 32
+    chunk = _descriptors([lens[b] for b in keep], [[(lens[b] - 16, 16)] if i == 0 else [(lens[b] - 1, 1)]
+                                                   for i, b in enumerate(keep)],
+                         heads["num_q_heads"], heads["num_kv_heads"], heads["head_dim"])
+    assert host_plan(msa, chunk).info()["tile_rows"] == 128
     assert host_plan(msa, make_layout_only(2), flags=msa.MSA_PLAN_TILE_ROWS_128).info()["tile_rows"] == 128
+
+
+def test_decode_split_fits_one_round(msa):
+    """32-row plans cut their units at the shortest 64-aligned length whose
+    pieces all fit one round of the 512 workgroup slots (two per CU)."""
+    _, layout = workloads.CONFIGS[5]
+    lens, segs, heads = layout(np.random.Generator(np.random.PCG64(5)))
+    keep = [b for b in range(len(lens)) if segs[b] == [(lens[b] - 1, 1)]]
+    decode = _descriptors([lens[b] for b in keep], [segs[b] for b in keep], heads["num_q_heads"],
+                          heads["num_kv_heads"], heads["head_dim"])
+    plan = host_plan(msa, decode)
+    _, work, _ = msa.msa_plan_export(plan)
+    assert plan.info()["tile_rows"] == 32
+    slots = 2 * 256
+    units = [lens[b] for b in keep for _ in range(heads["num_kv_heads"])]
+    count = lambda n: sum(-(-u // n) for u in units)
+    longest = int((work[:, 5] - work[:, 4]).max())
+    assert len(work) == count(longest) <= slots
+    assert longest % 64 == 0 and count(longest - 64) > slots
+    # more units than slots: no split
+    many = _descriptors([2000] * 200, [[(1999, 1)]] * 200, 32, 8, 128)
+    p2 = host_plan(msa, many)
+    assert p2.info()["tile_rows"] == 32 and p2.info()["num_merge"] == 0
 
 
 def test_one_hip_runtime_per_process():

@@ -59,8 +59,8 @@ RANDOM = [
 ]
 
 
-# plan flags: automatic tile width, forced 128-row tiles, forced 256-row tiles
-TILES = [0, msa.MSA_PLAN_TILE_ROWS_128, msa.MSA_PLAN_TILE_ROWS_256]
+# plan flags: automatic tile width, forced 128-row, 256-row and 32-row tiles
+TILES = [0, msa.MSA_PLAN_TILE_ROWS_128, msa.MSA_PLAN_TILE_ROWS_256, msa.MSA_PLAN_TILE_ROWS_32]
 
 
 @pytest.mark.parametrize("tile", TILES)

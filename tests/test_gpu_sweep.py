@@ -10,11 +10,10 @@ Each case draws its own shape and plan options:
 - contexts up to 1500 keys, 0-8 segments per sequence, at arbitrary or
   block-aligned boundaries;
 - forced key splits of 64-320 keys or none;
-- automatic, 128-row or 256-row tiles.
+- automatic, 128-row, 256-row or 32-row tiles.
 
-The bar is the same as the other parity tests.  Seed 141 holds a row at
-position 1 whose bf16 output lands 0.0102 from the oracle, 0.0024 beyond
-the rounding interval of the stored number (see ``tolerance.py``).
+The bar is the same as the other parity tests (see ``tolerance.py`` for
+how the max-abs bar treats the output's own bf16 rounding).
 """
 import numpy as np
 import pytest
@@ -33,7 +32,7 @@ import paper_2606_02964_amd as msa  # noqa: E402
 
 GROUPS = [1, 2, 3, 4, 5, 7, 8, 12, 16]
 SPLITS = [0, 0, 64, 128, 320]
-TILES = [0, msa.MSA_PLAN_TILE_ROWS_128, msa.MSA_PLAN_TILE_ROWS_256]
+TILES = [0, msa.MSA_PLAN_TILE_ROWS_128, msa.MSA_PLAN_TILE_ROWS_256, msa.MSA_PLAN_TILE_ROWS_32]
 
 
 def _case(seed):

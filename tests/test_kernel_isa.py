@@ -5,7 +5,8 @@ change could silently undo.  These tests compile the sources the way the
 build does and check them in the assembly and the resource report:
 
 * no kernel spills registers or uses scratch memory;
-* the attention kernels keep two waves per SIMD (their tiles assume it);
+* the attention kernels keep two waves per SIMD (their tiles assume it;
+  32-row tiles need two workgroups per CU);
 * in the attention kernels the MFMA operand reads run ahead: most LDS waits
   leave later reads outstanding (``lgkmcnt(N)`` with N >= 1).  When the
   compiler sees the global-to-LDS copies it waits for every LDS read before
@@ -73,8 +74,9 @@ def test_no_spills_or_scratch(compiled, src):
 
 
 def test_attention_occupancy(compiled):
-    kernels = {k: v for k, v in _resources(compiled["attn.hip"][1]).items() if "msa_attn_kernel" in k}
-    assert len(kernels) == 4  # d in {64, 128} x {4, 8} waves
+    kernels = {k: v for k, v in _resources(compiled["attn.hip"][1]).items()
+               if "msa_attn_kernel" in k or "msa_decode_kernel" in k}
+    assert len(kernels) == 6  # d in {64, 128} x {4, 8 waves, 32-row tiles}
     for name, r in kernels.items():
         assert r["Occupancy"] >= 2, (name, r)
 
