@@ -31,6 +31,9 @@
 // QK MFMAs of step j+1 are interleaved with the exponentials of step j, so
 // that each of them is followed by independent vector work.  The diagonal
 // steps and the last one run the same operations without overlap.
+// msa_decode: 32-row tiles of decode-like plans; the four waves of a
+// workgroup split the tile's keys, read K and V straight into registers and
+// merge their softmax states through LDS (see the kernel).
 // msa_merge: combines the per-split partials of a split tile by log-sum-exp.
 #include <hip/hip_runtime.h>
 
