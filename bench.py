@@ -424,6 +424,9 @@ def main():
     ap.add_argument("--cold", action="store_true",
                     help="also time calls after flushing L2 and the infinity cache (extra launches)")
     ap.add_argument("--kv-split-tokens", type=int, default=0)
+    ap.add_argument("--decode-only", action="store_true",
+                    help="keep only the decode rows of the workload (the sequences whose one segment is their "
+                         "last token); the roofline is then HBM-bound")
     ap.add_argument("--report", metavar="PATH", default=None,
                     help="only time every named workload and write one JSON line per case to PATH")
     ap.add_argument("--fused-ablation", metavar="PATH", default=None,
@@ -471,7 +474,9 @@ def main():
 
     cfg = args.workload
     t0 = time.perf_counter()
-    inst = workloads.make_config(cfg, seed=args.seed)
+    inst = workloads.make_config(cfg, seed=args.seed, decode_only=args.decode_only)
+    if inst.total_q == 0:
+        raise SystemExit(f"workload {cfg} has no rows to time")
     log(f"workload {cfg} generated in {time.perf_counter() - t0:.1f} s: total_q={inst.total_q}, "
         f"segments={len(inst.seg_len)}")
     q, k, v = dev_bf16(inst.q), dev_bf16(inst.k_cache), dev_bf16(inst.v_cache)
@@ -523,10 +528,18 @@ def main():
     useful = info["useful_flops"]
     achieved = useful / (ms * 1e-3) / 1e12
     workload_name = workloads.CONFIG_DESCRIPTIONS[cfg] + f" (seed {cfg if args.seed is None else args.seed})"
-    traffic = measured_traffic(workload_name) if info["num_merge"] == 0 else None
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic}
+    if args.decode_only:
+        # decode rows: bound by streaming their visible K/V once (per call,
+        # the split merge included)
+        workload_name += ", decode rows only"
+        gbs = info["min_bytes"] / (ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None}
+    else:
+        traffic = measured_traffic(workload_name) if info["num_merge"] == 0 else None
+        roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                    "traffic": traffic}
 
     cpu = None
     if not args.no_cpu_baseline:
