@@ -138,16 +138,19 @@ def _sample_items(inst, n, seed):
 
 
 @pytest.mark.parametrize("split", [0, 4096])
-def test_decode_tiles_long_unsplit_rows(oracle_lib, split):
+@pytest.mark.parametrize("hq,hkv,d", [(16, 2, 128), (16, 2, 64), (32, 1, 128)])
+def test_decode_tiles_long_unsplit_rows(oracle_lib, split, hq, hkv, d):
     """32-row tiles over long key ranges.  Without splits a wave of a tile
     covering 50000 keys runs 391 half-steps, past the 64 whose block ids it
     loads up front, so it also reads ids from the table as it goes.  Rows:
     decode rows at several context lengths (one ending mid-block), two
-    tokens of one sequence (a causal mask inside the last half-step) and a
-    G = 8 group."""
+    tokens of one sequence (a causal mask inside the last half-step); groups
+    of 8 and of 32 heads (one token fills a tile), d = 128 and 64."""
     kv = [50000, 8193, 12345, 40, 17]
     segs = [[(49999, 1)], [(8192, 1)], [(12343, 2)], [(39, 1)], [(16, 1)]]
-    inst = workloads.make_layout(77, kv, segs, 16, 2, 128, keep_logical=False)
+    if hq // hkv == 32:
+        segs[2] = [(12344, 1)]  # two tokens x 32 heads would not fit a 32-row tile
+    inst = workloads.make_layout(77, kv, segs, hq, hkv, d, keep_logical=False)
     flags = msa.MSA_PLAN_TILE_ROWS_32 | (msa.MSA_PLAN_NO_AUTO_SPLIT if split == 0 else 0)
     _, _, plan = check_full(inst, oracle_lib, kv_split_tokens=split, flags=flags)
     assert plan.info()["tile_rows"] == 32
