@@ -531,6 +531,38 @@ def test_decode_split_fits_one_round(msa):
     assert p2.info()["tile_rows"] == 32 and p2.info()["num_merge"] == 0
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_decode_split_rule_on_random_batches(msa, seed):
+    """Random decode batches: the pieces of a 32-row plan fit one round of
+    the 512 workgroup slots whenever the units alone do, and no shorter
+    64-aligned cut (above the 1024-key floor) would still fit."""
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 96))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 4, 8]))
+    lens = [int(x) for x in rng.integers(1, 40000, size=B)]
+    inst = _descriptors(lens, [[(L - 1, 1)] for L in lens], G * hkv, hkv, 128)
+    plan = host_plan(msa, inst)
+    info = plan.info()
+    assert info["tile_rows"] == 32
+    _, work, _ = msa.msa_plan_export(plan)
+    work = work[work[:, 3] > 0]  # padding items (empty, they exit at once) even out the XCD queues
+    units = [L for L in lens for _ in range(hkv)]
+    slots = 512
+    if len(units) > slots:
+        assert info["num_merge"] == 0 and len(work) == len(units)
+        return
+    assert len(work) <= slots
+    if info["num_merge"]:
+        # every piece is at most the cut length, so rounding the longest one
+        # up to 64 keys gives at most the cut; one step shorter must not fit
+        longest = int((work[:, 5] - work[:, 4]).max())
+        at_most_cut = -(-longest // 64) * 64
+        count = lambda n: sum(-(-u // n) for u in units)
+        if at_most_cut - 64 >= 1024:
+            assert count(at_most_cut - 64) > slots
+
+
 def test_one_hip_runtime_per_process():
     """Importing the package before torch must not load a second HIP runtime
     (torch's streams and device pointers belong to torch's runtime)."""
