@@ -124,6 +124,30 @@ def time_calls(step, stream, warmup, steps):
     return a.elapsed_time(b) / steps
 
 
+def gather_rates(inst, k, v, stream, warmup, steps):
+    """Read+write GB/s of torch's index_select copying the K and V cache blocks
+    the rows see, taken from their (random) places in the pool, beside the same
+    number of blocks copied from one contiguous range of the pool: the rate a
+    plain gather reaches on this block placement, for comparison with the
+    attention kernel's read rate."""
+    import numpy as np
+    import torch
+    nb = (inst.seq_kv_len.astype(np.int64) + 15) // 16
+    ids = np.concatenate([inst.block_table[s, :nb[s]] for s in range(inst.num_seqs)]).astype(np.int64)
+    kf, vf = k.view(inst.num_blocks, -1), v.view(inst.num_blocks, -1)
+    dk = torch.empty((len(ids), kf.shape[1]), dtype=k.dtype, device="cuda")
+    dv = torch.empty_like(dk)
+    nbytes = 2 * 2 * dk.numel() * dk.element_size()  # K and V, read and written
+    out = {"blocks": int(len(ids)), "bytes_read": nbytes // 2}
+    for name, idx in (("random", torch.from_numpy(ids).cuda()),
+                      ("contiguous", torch.arange(len(ids), device="cuda"))):
+        def step():
+            torch.index_select(kf, 0, idx, out=dk)
+            torch.index_select(vf, 0, idx, out=dv)
+        out[name + "_gbs"] = round(nbytes / (time_calls(step, stream, warmup, steps) * 1e-3) / 1e9, 1)
+    return out
+
+
 REPORT_CASES = [
     # (label, workload, make_config keyword arguments)
     ("tiny", 1, {}),
@@ -535,6 +559,8 @@ def main():
         gbs = info["min_bytes"] / (ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None}
+        gather = gather_rates(inst, k, v, stream, args.warmup, args.steps)
+        log(f"plain gather of the same blocks: {gather}")
     else:
         traffic = measured_traffic(workload_name) if info["num_merge"] == 0 else None
         roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
@@ -579,6 +605,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if args.decode_only:
+        out["gather_copy"] = gather
     print(json.dumps(out), flush=True)
 
 
