@@ -157,7 +157,8 @@ def test_decode_tiles_long_unsplit_rows(oracle_lib, split, hq, hkv, d):
     assert (plan.info()["num_merge"] > 0) == (split > 0)
 
 
-@pytest.mark.parametrize("tile", [msa.MSA_PLAN_TILE_ROWS_128, msa.MSA_PLAN_TILE_ROWS_256])
+@pytest.mark.parametrize("tile", [msa.MSA_PLAN_TILE_ROWS_128, msa.MSA_PLAN_TILE_ROWS_256,
+                                  msa.MSA_PLAN_TILE_ROWS_32])
 def test_scores_that_start_far_below_and_jump(oracle_lib, tile):
     """Score ranges that exercise the reference max: a rank-one bias along a
     unit vector u puts each sequence's first 64 keys about 150 (log2 units)
@@ -291,22 +292,24 @@ def test_config4_forced_split_matches_unsplit(oracle_lib):
     assert mx <= MAX_ABS and mean <= MEAN_ABS
 
 
-def test_physical_permutation_is_bitwise_invariant():
+@pytest.mark.parametrize("tile", [0, msa.MSA_PLAN_TILE_ROWS_32])
+def test_physical_permutation_is_bitwise_invariant(tile):
     inst = workloads.make_random(201, num_seqs=3, num_q_heads=32, num_kv_heads=8, head_dim=128,
                                  max_len=1500, max_segs=6, keep_logical=False, extra_blocks=5)
-    o1, l1, _ = run(DeviceInstance(inst))
-    o2, l2, _ = run(DeviceInstance(repermute(inst, 5)))
+    o1, l1, _ = run(DeviceInstance(inst), flags=tile)
+    o2, l2, _ = run(DeviceInstance(repermute(inst, 5)), flags=tile)
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
     assert torch.equal(l1, l2)
 
 
-def test_unreferenced_poison_and_garbage_past_context_end():
+@pytest.mark.parametrize("tile", [0, msa.MSA_PLAN_TILE_ROWS_32])
+def test_unreferenced_poison_and_garbage_past_context_end(tile):
     """NaN in blocks no table references and huge finite values past the
     context end inside referenced blocks leave every output bit unchanged."""
     inst = workloads.make_random(202, num_seqs=3, num_q_heads=8, num_kv_heads=2, head_dim=128,
                                  min_len=100, max_len=700, max_segs=4, keep_logical=False,
                                  extra_blocks=4)
-    o1, l1, _ = run(DeviceInstance(inst))
+    o1, l1, _ = run(DeviceInstance(inst), flags=tile)
     bad = copy.copy(inst)
     bad.k_cache = inst.k_cache.copy()
     bad.v_cache = inst.v_cache.copy()
@@ -323,7 +326,7 @@ def test_unreferenced_poison_and_garbage_past_context_end():
             blk = inst.block_table[b, L // 16]
             bad.k_cache[blk, :, L % 16:, :] = big
             bad.v_cache[blk, :, :, L % 16:] = big
-    o2, l2, _ = run(DeviceInstance(bad))
+    o2, l2, _ = run(DeviceInstance(bad), flags=tile)
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
     assert torch.equal(l1, l2)
 
@@ -442,7 +445,8 @@ def test_large_query_groups(oracle_lib, hq, hkv, d, tile):
     assert plan.info()["tile_rows"] == expect
 
 
-def test_hip_graph_replays_match_eager():
+@pytest.mark.parametrize("tile", [0, msa.MSA_PLAN_TILE_ROWS_32])
+def test_hip_graph_replays_match_eager(tile):
     """msa_kv_append and msa_forward (with key splits, so the merge kernel
     runs too) allocate and clear nothing, so a serving loop can capture them
     in a HIP graph.  Every replay, with eager work and synchronisation in
@@ -450,7 +454,7 @@ def test_hip_graph_replays_match_eager():
     inst = workloads.make_random(211, num_seqs=3, num_q_heads=16, num_kv_heads=4, head_dim=128,
                                  max_len=1500, max_segs=5, keep_logical=False)
     d = DeviceInstance(inst)
-    plan = d.plan(kv_split_tokens=256)
+    plan = d.plan(kv_split_tokens=256, flags=tile)
     info = plan.info()
     assert info["num_merge"] > 0
     kn, vn = (dev_bf16(x) for x in workloads.make_fresh_kv(inst, 5))
