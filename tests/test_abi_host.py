@@ -140,7 +140,7 @@ PLAN_CASES = [
 
 @pytest.mark.parametrize("case", PLAN_CASES)
 @pytest.mark.parametrize("split", [0, 64, 192, 1024])
-@pytest.mark.parametrize("tile_flag", [0, 4, 8])  # auto, 128-row, 256-row tiles
+@pytest.mark.parametrize("tile_flag", [0, 4, 8, 16])  # auto, 128-row, 256-row, 32-row tiles
 def test_plan_structure(msa, case, split, tile_flag):
     inst = workloads.make_random(keep_logical=False, **case)
     plan = host_plan(msa, inst, kv_split_tokens=split, flags=tile_flag)
@@ -386,7 +386,7 @@ def interpret_plan(inst, row_pos, work, merge):
     return out_o, out_l
 
 
-@pytest.mark.parametrize("tile_flag", [4, 8])
+@pytest.mark.parametrize("tile_flag", [4, 8, 16])
 @pytest.mark.parametrize("split", [0, 64, 128])
 @pytest.mark.parametrize("case", PLAN_CASES[:2] + PLAN_CASES[3:])
 def test_plan_interpreter_matches_oracle(msa, oracle_lib, case, split, tile_flag):
