@@ -197,17 +197,22 @@ def test_scores_that_start_far_below_and_jump(oracle_lib, tile):
     assert float(np.abs(lse.cpu().numpy().astype(np.float64) - rl).max()) <= bound
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4, 5, "5-decode"])
-def test_named_workload_sampled_parity(oracle_lib, cfg):
+@pytest.mark.parametrize("cfg,tile", [(2, 0), (3, 0), (4, 0), (5, 0), ("5-decode", 0),
+                                      (3, msa.MSA_PLAN_TILE_ROWS_32), (5, msa.MSA_PLAN_TILE_ROWS_32)])
+def test_named_workload_sampled_parity(oracle_lib, cfg, tile):
     """Full-size workloads in the benchmark's launch configuration (automatic
-    plan): every output finite and inside the convex hull of V, sampled
+    plan; two of them also forced onto 32-row tiles, whose kernel then takes
+    prefill segments at full size): every output finite and inside the
+    convex hull of V, sampled
     (row, head) items against the oracle."""
     if cfg == "5-decode":
         inst, cfg = workloads.make_config(5, decode_only=True), 6
     else:
         inst = workloads.make_config(cfg)
     d = DeviceInstance(inst)
-    o, lse, plan = run(d)
+    o, lse, plan = run(d, flags=tile)
+    if tile:
+        assert plan.info()["tile_rows"] == 32
     go = o.float()
     assert torch.isfinite(go).all().item(), "some output rows were not written"
     assert torch.isfinite(lse).all().item()
