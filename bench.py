@@ -394,8 +394,9 @@ def evictor_bench(path: str):
     trace on an 8192-block cache (300 conversations x 8 turns = 2400
     requests) is recorded once.  It is then replayed through the library's
     two-tree evictor and through its O(n) scan, which must evict the same
-    blocks.  The oracle replays it too, for parity (its time is reported as
-    the plain-definition baseline).  Host-only; one JSON line to `path`."""
+    blocks.  As the CPU baseline, the oracle replays it too (its time is the
+    plain-definition baseline, and its evictions must agree).  Host-only;
+    one JSON line to `path`."""
     import numpy as np
     import oracle
     import workloads
@@ -423,6 +424,8 @@ def evictor_bench(path: str):
         rec[f"{name}_us_per_op"] = round(dt / trace.op.size * 1e6, 4)
         rec[f"{name}_us_per_eviction"] = round(dt / max(1, ev.sum()) * 1e6, 3)
         rec[f"{name}_ms_per_request"] = round(dt / trace.requests * 1e3, 4)
+    # CPU-baseline leg: the oracle's plain O(n)-scan replay of the same trace,
+    # timed; its evictions must be the library's
     t0 = time.perf_counter()
     ref = oracle.evictor_replay(params["alpha"], params["beta"], params["tau0"], 1.0,
                                 trace.op, trace.ids, trace.t, trace.cost)
