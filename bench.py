@@ -468,7 +468,7 @@ def main():
 
     if args.gpus != 1:
         print("bench.py: this build runs on exactly one GPU; --gpus must be 1 "
-              "(multi-GPU sharding is described in DESIGN.md, not implemented)", file=sys.stderr)
+              "(sharding over several GPUs is designed, not implemented)", file=sys.stderr)
         sys.exit(2)
 
     if args.evictor:
