@@ -467,7 +467,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print("bench.py: this build runs on exactly one GPU; --gpus must be 1 "
+        print("bench.py: this benchmark runs on exactly one GPU; --gpus must be 1 "
               "(sharding over several GPUs is designed, not implemented)", file=sys.stderr)
         sys.exit(2)
 
