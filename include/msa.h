@@ -43,14 +43,20 @@
  *    immutable, serves every layer of one batch step, and msa_forward may be
  *    called with it concurrently on different streams provided each call has
  *    its own workspace and output.
- *  - Errors: every function returns a status; MSA_OK is 0.  On any other
- *    status nothing was launched and no output was written;
- *    msa_last_error() then returns a thread-local message.
+ *  - Errors: every function returns a status; MSA_OK is 0.  On
+ *    MSA_ERR_INVALID_ARG, MSA_ERR_UNSUPPORTED and MSA_ERR_OUT_OF_MEMORY
+ *    nothing was launched and no output was written.  MSA_ERR_DEVICE means
+ *    a HIP call or launch failed: work enqueued before it in the same call
+ *    (msa_forward's attention launch, when its merge launch fails) may have
+ *    written part of the output.  msa_last_error() then returns a
+ *    thread-local message.
  *  - Preconditions not checked on the hot path: the K/V of every query
  *    position are already in the cache; block_table[b][i] is a valid
  *    physical block for every i < ceil((max query position of b + 1) / bs);
  *    other block-table entries are never read; cache values at positions
- *    >= seq_kv_len[b] inside a referenced block are finite.
+ *    >= seq_kv_len[b] inside a referenced block are finite.  An entry outside
+ *    [0, num_blocks) makes the kernels read outside the caches;
+ *    msa_check_block_table validates a table against a plan (debug use).
  */
 #ifndef MSA_H_
 #define MSA_H_
@@ -136,6 +142,14 @@ typedef struct msa_plan_info_t {
 /*
  * msa_plan: validate the segment descriptors and build the work list.
  *
+ * The paper runs the attention of all segments of all requests in one
+ * kernel, handing it the segments' split indices; each query token finds its
+ * "equivalent seq_len" (its causal limit) in a precomputed per-token array
+ * (Sec. 4.1, Eq. 2).  msa_plan builds both once per batch step: the split
+ * indices are seg_indptr / seg_start / seg_len, the per-token array is the
+ * plan's row-position table (msa_plan_export), and the work list maps tiles
+ * of query rows x KV heads x key ranges onto workgroups.
+ *
  *   shape       problem shape and strides (host pointer, read during the call)
  *   seq_kv_len  [num_seqs] host: context length of each sequence, 0 <= L <=
  *               max_blocks_per_seq * block_size
@@ -165,7 +179,12 @@ msa_status msa_plan(const msa_shape *shape, const int32_t *seq_kv_len, const int
 msa_status msa_plan_info(msa_plan_t plan, msa_plan_info_t *info);
 
 /*
- * msa_forward: run MSA for one layer.
+ * msa_forward: run MSA for one layer: the attention of every packed query
+ * row over the keys at positions 0..p of its sequence (Sec. 4.1, Eq. 2, on
+ * attention as in Sec. 2.1, Eq. 1), read from the paged cache through the
+ * block table (the kernel extends PagedAttention, Sec. 5.3), as one fused
+ * launch for all segments (plus a log-sum-exp merge launch when the plan
+ * split long key ranges).
  *
  *   q            device bf16 [total_q, Hq, d] (strided as in the shape)
  *   k_cache      device bf16, token-major blocks (see conventions)
@@ -179,7 +198,9 @@ msa_status msa_plan_info(msa_plan_t plan, msa_plan_info_t *info);
  *   hip_stream   hipStream_t on which all kernels are enqueued (no host sync)
  *
  * Returns MSA_ERR_INVALID_ARG for NULL or misaligned pointers, a too-small
- * workspace or a host-only plan; MSA_ERR_DEVICE if a launch fails.
+ * workspace or a host-only plan; MSA_ERR_DEVICE if a launch fails (if the
+ * merge launch fails, the attention launch before it may have written part
+ * of o and lse).  The block table is not checked (see msa_check_block_table).
  */
 msa_status msa_forward(msa_plan_t plan, const void *q, const void *k_cache, const void *v_cache,
                        const int32_t *block_table, void *o, float *lse, void *workspace,
@@ -217,6 +238,37 @@ msa_status msa_kv_append(msa_plan_t plan, const void *k_new, const void *v_new,
                          int64_t v_new_stride_tok, int64_t v_new_stride_head,
                          const int32_t *block_table, void *k_cache, void *v_cache,
                          void *hip_stream);
+
+/*
+ * msa_check_block_table: debug-only validation of a block table against a
+ * plan, before msa_forward or msa_kv_append use it.  The paged cache of
+ * PagedAttention (Sec. 5.3) maps each sequence's logical blocks to physical
+ * ones; the kernels trust that mapping, and an entry outside [0, num_blocks)
+ * makes them read (or, for msa_forward, fault) outside the caches.
+ *
+ * Reads exactly the entries the plan's kernels read: for sequence b,
+ * logical blocks 0 .. ceil((P_b + 1) / block_size) - 1, where P_b is the
+ * largest query position of b (no entry if b has no query rows).
+ *
+ *   block_table  [num_seqs * max_blocks_per_seq] int32, row stride
+ *                max_blocks_per_seq (host or device memory, per location)
+ *   location     MSA_TABLE_HOST: a host pointer, read directly;
+ *                MSA_TABLE_DEVICE: a device pointer; the entries are copied
+ *                to the host on hip_stream, which is then synchronised (the
+ *                copy is ordered after earlier work on that stream)
+ *   hip_stream   hipStream_t for the copy (ignored for host tables)
+ *
+ * Works on host-only plans too.  Returns MSA_OK when every entry read lies
+ * in [0, num_blocks); MSA_ERR_INVALID_ARG for the first entry that does not,
+ * in sequence order then logical-block order, with msa_last_error() naming
+ * the sequence, the logical block and the value; MSA_ERR_INVALID_ARG for a
+ * NULL or misaligned table or a bad location; MSA_ERR_DEVICE if the copy
+ * fails; MSA_ERR_OUT_OF_MEMORY.  Nothing is written.
+ */
+#define MSA_TABLE_HOST 0
+#define MSA_TABLE_DEVICE 1
+msa_status msa_check_block_table(msa_plan_t plan, const int32_t *block_table, int32_t location,
+                                 void *hip_stream);
 
 /* msa_plan_destroy: free a plan.  The caller must have synchronised every
  * stream that used it.  NULL is accepted. */

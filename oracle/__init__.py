@@ -23,7 +23,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "msa_oracle.c")
 _SRC_EVICTOR = os.path.join(_HERE, "evictor_oracle.c")
-_LIB = os.path.join(_HERE, "libmsa_oracle.so")
+# MSA_ORACLE_LIBRARY names another build of the same oracle (the
+# host-sanitizer test loads an instrumented build this way)
+_LIB = os.environ.get("MSA_ORACLE_LIBRARY") or os.path.join(_HERE, "libmsa_oracle.so")
 _lib = None
 
 

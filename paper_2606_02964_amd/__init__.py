@@ -7,7 +7,7 @@ fallback: importing this package without a built library raises.
 
 Functions carry the C names: ``msa_plan``, ``msa_plan_info``,
 ``msa_forward``, ``msa_kv_append``, ``msa_plan_destroy``,
-``msa_last_error``, ``msa_plan_export``.  Device buffers are passed as objects with a
+``msa_last_error``, ``msa_plan_export``, ``msa_check_block_table``.  Device buffers are passed as objects with a
 ``data_ptr()`` method (e.g. torch tensors) or as integer addresses; streams
 as ``hipStream_t`` integers or objects with ``cuda_stream`` (torch streams).
 """
@@ -20,7 +20,9 @@ from typing import Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmsa.so")
+# MSA_LIBRARY names another build of the same library (the host-sanitizer
+# test loads an instrumented build of the planner this way)
+LIB_PATH = os.environ.get("MSA_LIBRARY") or os.path.join(_HERE, "libmsa.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_02964_amd.build`")
@@ -43,6 +45,8 @@ MSA_PLAN_NO_AUTO_SPLIT = 2
 MSA_PLAN_TILE_ROWS_128 = 4
 MSA_PLAN_TILE_ROWS_256 = 8
 MSA_PLAN_TILE_ROWS_32 = 16
+MSA_TABLE_HOST = 0
+MSA_TABLE_DEVICE = 1
 
 _i32, _i64, _f32, _f64, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 
@@ -87,6 +91,8 @@ _lib.msa_last_error.restype = ctypes.c_char_p
 _lib.msa_last_error.argtypes = []
 _lib.msa_plan_export.restype = _i32
 _lib.msa_plan_export.argtypes = [_P, _P, _P, _P]
+_lib.msa_check_block_table.restype = _i32
+_lib.msa_check_block_table.argtypes = [_P, _P, _i32, _P]
 
 _lib.msa_evictor_create.restype = _i32
 _lib.msa_evictor_create.argtypes = [_P, ctypes.POINTER(_P)]
@@ -110,7 +116,7 @@ _lib.msa_evictor_replay.restype = _i32
 _lib.msa_evictor_replay.argtypes = [_P, _i64, _P, _P, _P, _P, _P, ctypes.POINTER(_i64)]
 
 EXPORTED = ("msa_plan", "msa_plan_info", "msa_forward", "msa_kv_append", "msa_plan_destroy",
-            "msa_last_error", "msa_plan_export",
+            "msa_last_error", "msa_plan_export", "msa_check_block_table",
             "msa_evictor_create", "msa_evictor_destroy", "msa_evictor_add", "msa_evictor_remove",
             "msa_evictor_evict", "msa_evictor_set_lambda", "msa_evictor_set_lifespan",
             "msa_evictor_size", "msa_evictor_log_weight", "msa_evictor_replay")
@@ -214,6 +220,19 @@ def msa_plan_export(plan: Plan):
                                 work.ctypes.data if work.size else None,
                                 merge.ctypes.data if merge.size else None))
     return row_pos, work, merge
+
+
+def msa_check_block_table(plan: Plan, block_table, stream=None) -> None:
+    """Debug check of the block-table entries the plan reads (raises MsaError
+    naming the first bad entry).  A numpy array is checked as a host table,
+    anything else (a device tensor, an integer address) as a device table."""
+    if isinstance(block_table, np.ndarray):
+        bt = np.ascontiguousarray(block_table, dtype=np.int32)
+        _check(_lib.msa_check_block_table(plan.handle, bt.ctypes.data if bt.size else None,
+                                          MSA_TABLE_HOST, None))
+    else:
+        _check(_lib.msa_check_block_table(plan.handle, _addr(block_table), MSA_TABLE_DEVICE,
+                                          _stream(stream)))
 
 
 def msa_forward(plan: Plan, q, k_cache, v_cache, block_table, o, lse=None, workspace=None,

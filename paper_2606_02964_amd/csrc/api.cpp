@@ -1,6 +1,7 @@
 // api.cpp -- the C ABI declared in include/msa.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <new>
@@ -10,6 +11,7 @@
 #include "msa.h"
 #include "append.h"
 #include "errors.h"
+#include "forward.h"
 #include "msa_internal.h"
 #include "plan.h"
 
@@ -41,6 +43,79 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 }  // namespace
 
 void msa::set_last_error(const std::string& msg) { g_last_error = msg; }
+
+msa_status msa::forward_impl(const char* who, msa_plan_t plan, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* block_table, void* o, float* lse,
+                        void* workspace, size_t workspace_bytes, void* hip_stream) {
+  const std::string w(who);
+  if (!plan) return set_error(MSA_ERR_INVALID_ARG, w + ": null plan");
+  if (plan->host_only)
+    return set_error(MSA_ERR_INVALID_ARG, w + ": plan was built with MSA_PLAN_HOST_ONLY");
+  const msa::HostPlan& hp = plan->hp;
+  if (hp.work.empty()) return MSA_OK;  // no query rows: nothing to do
+  if (!q || !k_cache || !v_cache || !block_table || !o)
+    return set_error(MSA_ERR_INVALID_ARG, w + ": q, k_cache, v_cache, block_table, o must be non-null");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(o, 16) ||
+      !aligned(block_table, 4) || (lse && !aligned(lse, 4)))
+    return set_error(MSA_ERR_INVALID_ARG, w + ": q/k/v/o must be 16-byte aligned");
+  if ((size_t)hp.workspace_bytes > workspace_bytes)
+    return set_error(MSA_ERR_INVALID_ARG,
+                     w + ": workspace too small (need " + std::to_string(hp.workspace_bytes) +
+                         " bytes)");
+  if (hp.workspace_bytes > 0 && (!workspace || !aligned(workspace, 16)))
+    return set_error(MSA_ERR_INVALID_ARG, w + ": workspace must be non-null and 16-byte aligned");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
+    return set_error(MSA_ERR_INVALID_ARG, w + ": current device differs from the plan's device");
+
+  const msa_shape& s = hp.shape;
+  msa::AttnParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_cache);
+  p.v = static_cast<const uint16_t*>(v_cache);
+  p.block_table = block_table;
+  p.row_pos = plan->d_row_pos;
+  p.work = plan->d_work;
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.ws = static_cast<float*>(workspace);
+  p.q_st = s.q_stride_tok;
+  p.q_sh = s.q_stride_head;
+  p.o_st = s.o_stride_tok;
+  p.o_sh = s.o_stride_head;
+  p.k_sb = s.k_stride_block;
+  p.k_sh = s.k_stride_head;
+  p.k_st = s.k_stride_tok;
+  p.v_sb = s.v_stride_block;
+  p.v_sh = s.v_stride_head;
+  p.v_sd = s.v_stride_dim;
+  p.max_blocks = s.max_blocks_per_seq;
+  p.num_q_heads = s.num_q_heads;
+  p.group = hp.group;
+  p.tile_tokens = hp.tile_tokens;
+  p.scale_log2 = s.scale * 1.4426950408889634f;
+  int rc = msa::launch_attn(p, s.head_dim, hp.tile_rows, (int)hp.work.size(), hip_stream);
+  if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string(w + ": attention launch failed: ") +
+                                                    hipGetErrorString((hipError_t)rc));
+  if (!hp.merge.empty()) {
+    msa::MergeParams m{};
+    m.merge = plan->d_merge;
+    m.ws = static_cast<const float*>(workspace);
+    m.o = static_cast<uint16_t*>(o);
+    m.lse = lse;
+    m.o_st = s.o_stride_tok;
+    m.o_sh = s.o_stride_head;
+    m.num_q_heads = s.num_q_heads;
+    m.group = hp.group;
+    m.tile_rows = hp.tile_rows;
+    rc = msa::launch_merge(m, s.head_dim, (int)hp.merge.size(), hip_stream);
+    if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string(w + ": merge launch failed: ") +
+                                                      hipGetErrorString((hipError_t)rc));
+  }
+  return MSA_OK;
+}
+
+int64_t msa::plan_workspace_bytes(msa_plan_t plan) { return plan->hp.workspace_bytes; }
 
 extern "C" {
 
@@ -152,69 +227,54 @@ void msa_plan_destroy(msa_plan_t plan) {
 msa_status msa_forward(msa_plan_t plan, const void* q, const void* k_cache, const void* v_cache,
                        const int32_t* block_table, void* o, float* lse, void* workspace,
                        size_t workspace_bytes, void* hip_stream) {
-  if (!plan) return set_error(MSA_ERR_INVALID_ARG, "msa_forward: null plan");
-  if (plan->host_only)
-    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: plan was built with MSA_PLAN_HOST_ONLY");
-  const msa::HostPlan& hp = plan->hp;
-  if (hp.work.empty()) return MSA_OK;  // no query rows: nothing to do
-  if (!q || !k_cache || !v_cache || !block_table || !o)
-    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: q, k_cache, v_cache, block_table, o must be non-null");
-  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(o, 16) ||
-      !aligned(block_table, 4) || (lse && !aligned(lse, 4)))
-    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: q/k/v/o must be 16-byte aligned");
-  if ((size_t)hp.workspace_bytes > workspace_bytes)
-    return set_error(MSA_ERR_INVALID_ARG,
-                     "msa_forward: workspace too small (need " + std::to_string(hp.workspace_bytes) +
-                         " bytes)");
-  if (hp.workspace_bytes > 0 && (!workspace || !aligned(workspace, 16)))
-    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: workspace must be non-null and 16-byte aligned");
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
-    return set_error(MSA_ERR_INVALID_ARG, "msa_forward: current device differs from the plan's device");
+  return msa::forward_impl("msa_forward", plan, q, k_cache, v_cache, block_table, o, lse, workspace,
+                           workspace_bytes, hip_stream);
+}
 
+msa_status msa_check_block_table(msa_plan_t plan, const int32_t* block_table, int32_t location,
+                                 void* hip_stream) {
+  if (!plan) return set_error(MSA_ERR_INVALID_ARG, "msa_check_block_table: null plan");
+  if (location != MSA_TABLE_HOST && location != MSA_TABLE_DEVICE)
+    return set_error(MSA_ERR_INVALID_ARG, "msa_check_block_table: location must be MSA_TABLE_HOST or MSA_TABLE_DEVICE");
+  const msa::HostPlan& hp = plan->hp;
   const msa_shape& s = hp.shape;
-  msa::AttnParams p{};
-  p.q = static_cast<const uint16_t*>(q);
-  p.k = static_cast<const uint16_t*>(k_cache);
-  p.v = static_cast<const uint16_t*>(v_cache);
-  p.block_table = block_table;
-  p.row_pos = plan->d_row_pos;
-  p.work = plan->d_work;
-  p.o = static_cast<uint16_t*>(o);
-  p.lse = lse;
-  p.ws = static_cast<float*>(workspace);
-  p.q_st = s.q_stride_tok;
-  p.q_sh = s.q_stride_head;
-  p.o_st = s.o_stride_tok;
-  p.o_sh = s.o_stride_head;
-  p.k_sb = s.k_stride_block;
-  p.k_sh = s.k_stride_head;
-  p.k_st = s.k_stride_tok;
-  p.v_sb = s.v_stride_block;
-  p.v_sh = s.v_stride_head;
-  p.v_sd = s.v_stride_dim;
-  p.max_blocks = s.max_blocks_per_seq;
-  p.num_q_heads = s.num_q_heads;
-  p.group = hp.group;
-  p.tile_tokens = hp.tile_tokens;
-  p.scale_log2 = s.scale * 1.4426950408889634f;
-  int rc = msa::launch_attn(p, s.head_dim, hp.tile_rows, (int)hp.work.size(), hip_stream);
-  if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string("msa_forward: attention launch failed: ") +
-                                                    hipGetErrorString((hipError_t)rc));
-  if (!hp.merge.empty()) {
-    msa::MergeParams m{};
-    m.merge = plan->d_merge;
-    m.ws = static_cast<const float*>(workspace);
-    m.o = static_cast<uint16_t*>(o);
-    m.lse = lse;
-    m.o_st = s.o_stride_tok;
-    m.o_sh = s.o_stride_head;
-    m.num_q_heads = s.num_q_heads;
-    m.group = hp.group;
-    m.tile_rows = hp.tile_rows;
-    rc = msa::launch_merge(m, s.head_dim, (int)hp.merge.size(), hip_stream);
-    if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string("msa_forward: merge launch failed: ") +
-                                                      hipGetErrorString((hipError_t)rc));
+  int32_t width = 0;  // entries read per row: the most any sequence needs
+  for (int32_t nb : hp.seq_blocks) width = std::max(width, nb);
+  if (width == 0) return MSA_OK;  // the plan reads no entry
+  if (!block_table) return set_error(MSA_ERR_INVALID_ARG, "msa_check_block_table: null block_table");
+  if (!aligned(block_table, 4))
+    return set_error(MSA_ERR_INVALID_ARG, "msa_check_block_table: block_table must be 4-byte aligned");
+  const int32_t* table = block_table;
+  std::vector<int32_t> host;
+  if (location == MSA_TABLE_DEVICE) {
+    try {
+      host.assign((size_t)s.num_seqs * (size_t)width, 0);
+    } catch (const std::bad_alloc&) {
+      return set_error(MSA_ERR_OUT_OF_MEMORY, "msa_check_block_table: host allocation failed");
+    }
+    // the first `width` entries of every row, in one strided copy
+    hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    hipError_t e = hipMemcpy2DAsync(host.data(), (size_t)width * sizeof(int32_t), block_table,
+                                    (size_t)s.max_blocks_per_seq * sizeof(int32_t),
+                                    (size_t)width * sizeof(int32_t), (size_t)s.num_seqs,
+                                    hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return set_error(MSA_ERR_DEVICE, std::string("msa_check_block_table: copy of the table failed: ") +
+                                           hipGetErrorString(e));
+    }
+    table = host.data();
+  }
+  const int64_t row_stride = location == MSA_TABLE_DEVICE ? width : s.max_blocks_per_seq;
+  for (int32_t b = 0; b < s.num_seqs; ++b) {
+    const int32_t* row = table + (int64_t)b * row_stride;
+    for (int32_t i = 0; i < hp.seq_blocks[(size_t)b]; ++i)
+      if (row[i] < 0 || row[i] >= s.num_blocks)
+        return set_error(MSA_ERR_INVALID_ARG,
+                         "msa_check_block_table: sequence " + std::to_string(b) + ", logical block " +
+                             std::to_string(i) + " maps to physical block " + std::to_string(row[i]) +
+                             ", outside [0, " + std::to_string(s.num_blocks) + ")");
   }
   return MSA_OK;
 }

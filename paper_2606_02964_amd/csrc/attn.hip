@@ -26,14 +26,20 @@
 //   - O^T += V^T P^T on the same MFMA, P packed to bf16 straight from the
 //     score registers.  The A-operand row order of K is permuted (bits 2 and 3
 //     of the row index swapped) so that the 8 scores a lane feeds to one PV
-//     step are 8 consecutive keys, a single 16-byte LDS read of V^T.
+//     step are 8 consecutive keys, a single 16-byte LDS read of V^T.  On the
+//     step holding a row's own position (its latest keys, and all keys of a
+//     row near the start of a sequence) its weights enter as two bf16 terms,
+//     hi = bf16(w) and lo = bf16(w - hi), with a second PV pass on lo, and
+//     its row sum adds them in fp32: rows whose weight sits on a few keys
+//     then carry their weights to about 2^-18 instead of 2^-9.
 // Steps whose successor needs no mask run software-pipelined in pairs: the
 // QK MFMAs of step j+1 are interleaved with the exponentials of step j, so
 // that each of them is followed by independent vector work.  The diagonal
 // steps and the last one run the same operations without overlap.
 // msa_decode: 32-row tiles of decode-like plans; the four waves of a
 // workgroup split the tile's keys, read K and V straight into registers and
-// merge their softmax states through LDS (see the kernel).
+// merge their softmax states through LDS (see the kernel); masked
+// half-steps carry their weights as hi + lo terms, as above.
 // msa_merge: combines the per-split partials of a split tile by log-sum-exp.
 #include <hip/hip_runtime.h>
 
@@ -327,13 +333,43 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
       ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
     }
   };
+  // On the step that holds a row's own position (its diagonal step) the
+  // row's weights are carried as two bf16 terms: once the reference max is
+  // settled, w replaces each score in sbuf[b], the row sum is their fp32
+  // sum, and the PV product runs on hi = bf16(w) and on lo = bf16(w - hi)
+  // (w - hi is exact in fp32), so hi + lo is within 2^-18 of w.  The
+  // diagonal step holds a row's latest keys, and a row near the start of
+  // the sequence has all its keys there: few keys then carry all the
+  // weight, and a bf16 weight alone would move such a row's output by up to
+  // about 2^-9 |v_i - v_j|.  Which steps do this depends on the row's own
+  // position only (not on the rows sharing its wave), so a row's result
+  // does not depend on its tile.
+  auto weights_inplace = [&](int b, float& ls) {
+    const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
+    ls = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][e >> 4][e & 15], c, nm));
+      sbuf[b][e >> 4][e & 15] = x;
+      ls += x;
+    }
+  };
+  // packed bf16 lo terms of the weights e, e+1 held in sbuf[b], given their
+  // hi terms (zero for a row off its diagonal step: own = false)
+  auto lo_pair = [&](int b, int e, uint32_t hi, bool own) {
+    const bf16x2 h = __builtin_bit_cast(bf16x2, hi);
+    const uint32_t lo =
+        pack_bf16x2(sbuf[b][e >> 4][e & 15] - (float)h[0], sbuf[b][(e + 1) >> 4][(e + 1) & 15] - (float)h[1]);
+    return own ? lo : 0u;
+  };
   // The row max is only taken when the weights of a step may have outgrown
   // the reference: a lane's step sum reached 2^7, or the row has no
   // reference yet.  A row whose max exceeds the reference by more than 2^8
   // (in log2 units) holds a weight >= 2^8, so its lane's sum passes 2^7:
   // the reference moves exactly as if the max were taken every step.  The
   // weights are then recomputed against the new reference.
-  auto settle = [&](int b, uint32_t (&pk)[16], float& ls) {
+  // (reweigh recomputes the step's weights and their sum ls.)
+  auto settle = [&](int b, float ls, auto&& reweigh) {
     if (__any(!(ls < kSettleSum) || m_ref == -__builtin_inff())) {  // wave-uniform
       float mx = -__builtin_inff();
 #pragma unroll
@@ -346,7 +382,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
         l_run *= alpha;
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
-        weights_plain(b, pk, ls);
+        reweigh();
       }
     }
   };
@@ -393,7 +429,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    settle(B, pk, ls);
+    settle(B, ls, [&]() { weights_plain(B, pk, ls); });
     l_run += ls;
     // block 2
     const int lim = pos - (w.kv_lo + (j + 1) * kKvStep) - hl * 8;
@@ -424,7 +460,9 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   // barrier that ended iteration j-1 (the buffers' previous contents K_j and
   // V_{j-1} were last read before it) and waited for before the barrier that
   // ends iteration j.
-  auto need_mask = [&](int s) { return w.kv_lo + s * kKvStep + kKvStep - 1 > pmin; };
+  // (>=: a step whose last key is some row's position counts too, so that
+  // every row's diagonal step runs through the masked path)
+  auto need_mask = [&](int s) { return w.kv_lo + s * kKvStep + kKvStep - 1 >= pmin; };
   // steps this wave computes: keys up to its largest position.  A wave past
   // them still copies its share of every step and meets every barrier.
   const int nw = pmax >= w.kv_lo ? min(n, (pmax - w.kv_lo) / kKvStep + 1) : 0;
@@ -461,17 +499,38 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   // Remaining steps (the diagonal ones and the last) run without overlap:
   // weights of step j, PV of step j, then QK + mask of step j+1 into the
   // same score registers.  Same copy schedule as the pipelined loop.
-  auto plain = [&](int jj) {
+  // On a masked step (split: the diagonal step of some row of the wave) the
+  // rows whose diagonal step it is also enter their weights' bf16 lo terms
+  // (other rows: zeros), in a second PV pass after the usual one on pk.
+  auto plain = [&](int jj, bool split) {
     uint32_t pk[16];
     float ls;
     weights_plain(0, pk, ls);
-    settle(0, pk, ls);
+    settle(0, ls, [&]() { weights_plain(0, pk, ls); });
+    const int s_lo = w.kv_lo + jj * kKvStep;
+    const bool own = pos >= s_lo && pos < s_lo + kKvStep;  // this is the row's diagonal step
+    if (split) {  // the same weights in fp32, in place; hi(w) == pk
+      float lw;
+      weights_inplace(0, lw);
+      ls = own ? lw : ls;
+    }
     l_run += ls;
 #pragma unroll
     for (int i = 0; i < kPv; ++i) {
       const int ks = i / (D / 32), dt = i % (D / 32);
       const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
       oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vread(jj, i), pb, oacc[dt], 0, 0, 0);
+    }
+    if (split) {
+#pragma unroll
+      for (int i = 0; i < kPv; ++i) {
+        const int ks = i / (D / 32), dt = i % (D / 32);
+        uint32_t pl[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) pl[u] = lo_pair(0, 8 * ks + 2 * u, pk[4 * ks + u], own);
+        const bf16x8 pc = __builtin_bit_cast(bf16x8, make_uint4(pl[0], pl[1], pl[2], pl[3]));
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vread(jj, i), pc, oacc[dt], 0, 0, 0);
+      }
     }
     if (jj + 1 < nw) {
       qk_plain(0, jj + 1);
@@ -480,7 +539,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   };
   for (; j < n; ++j) {
     issue(j + 2, j + 1);
-    if (j < nw) plain(j);
+    if (j < nw) plain(j, need_mask(j));
     tail();
   }
 
@@ -651,7 +710,11 @@ __global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
     for (int kk = 0; kk < kQk; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[b][kk], qf[kk], sc, 0, 0, 0);
     // score e (0..15) of a lane is key (e / 8) * 16 + hl * 8 + e % 8 of the half-step
     const int k0 = w.kv_lo + h * kHalf;
-    if (k0 + kHalf - 1 > pmin) {
+    // On a masked half-step (split) the rows whose diagonal half-step it is
+    // also enter their weights' bf16 lo terms, as in the main kernel: a
+    // second PV pass on them follows.
+    const bool split = k0 + kHalf - 1 >= pmin;  // holds some row's position, or passes one
+    if (split) {
       const int lim = pos - k0 - hl * 8;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[e] = ((e >> 3) * 16 + (e & 7)) <= lim ? sc[e] : -__builtin_inff();
@@ -685,12 +748,37 @@ __global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
         weights();
       }
     }
+    const bool own = pos >= k0 && pos < k0 + kHalf;  // the row's diagonal half-step
+    if (split) {  // the same weights in fp32, in place of the scores; hi(w) == pk
+      const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
+      float lw = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        sc[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm));
+        lw += sc[e];
+      }
+      ls = own ? lw : ls;
+    }
     l_run += ls;
 #pragma unroll
     for (int i = 0; i < kPv; ++i) {
       const int ks = i / (D / 32), dt = i % (D / 32);
       const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
       oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pb, oacc[dt], 0, 0, 0);
+    }
+    if (split) {
+#pragma unroll
+      for (int i = 0; i < kPv; ++i) {
+        const int ks = i / (D / 32), dt = i % (D / 32);
+        uint32_t pl[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const bf16x2 hv = __builtin_bit_cast(bf16x2, pk[4 * ks + u]);
+          pl[u] = own ? pack_bf16x2(sc[8 * ks + 2 * u] - (float)hv[0], sc[8 * ks + 2 * u + 1] - (float)hv[1]) : 0u;
+        }
+        const bf16x8 pc = __builtin_bit_cast(bf16x8, make_uint4(pl[0], pl[1], pl[2], pl[3]));
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pc, oacc[dt], 0, 0, 0);
+      }
     }
   };
   if (wave < nhw) load_k(std::integral_constant<int, 0>{}, wave);

@@ -154,6 +154,8 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   }
   seq_row0[B] = total;
   P.total_q = total;
+  P.seq_blocks.resize((size_t)B);
+  for (int32_t b = 0; b < B; ++b) P.seq_blocks[(size_t)b] = seq_maxpos[b] >= 0 ? seq_maxpos[b] / kBlockSize + 1 : 0;
   P.row_pos.resize((size_t)total);
   {
     int64_t r = 0;

@@ -17,6 +17,7 @@ struct HostPlan {
   int32_t tile_tokens = 0;  // query tokens per tile
   int64_t total_q = 0;
   std::vector<int32_t> row_pos;   // [total_q] absolute position of each packed row
+  std::vector<int32_t> seq_blocks; // [num_seqs] block-table entries the plan reads per sequence
   std::vector<WorkItem> work;     // launch order (blockIdx.x)
   std::vector<MergeItem> merge;
   std::vector<AppendItem> append; // one per (segment, cache block) slice

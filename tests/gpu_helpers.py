@@ -2,11 +2,41 @@
 C ABI (via the thin binding).  GPU-only; imported by the ``-m gpu`` tests."""
 from __future__ import annotations
 
+import json
+import os
+
 import numpy as np
 import torch
 
 import paper_2606_02964_amd as msa
 from tolerance import LSE_ABS, MAX_ABS, MEAN_ABS, errors, raw_max_abs  # noqa: F401  (re-exported)
+
+
+def log_parity(**fields) -> None:
+    """Append one JSON line of parity figures (with the running test's id)
+    to the file named by MSA_PARITY_LOG, if set."""
+    path = os.environ.get("MSA_PARITY_LOG")
+    if not path:
+        return
+    fields["test"] = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    with open(path, "a") as f:
+        f.write(json.dumps(fields) + "\n")
+
+
+def check_o(go: np.ndarray, ro: np.ndarray, lse=None, rl=None, lse_tol: float = LSE_ABS) -> None:
+    """The O bar (max-abs per ``tolerance.py``, mean-abs) and, if given, the
+    lse bar; the plain max-abs over every element is logged beside them."""
+    go = np.asarray(go, dtype=np.float32)
+    mx, mean = errors(go, ro)
+    raw = raw_max_abs(go, ro)
+    lerr = None
+    if lse is not None:
+        lerr = float(np.abs(np.asarray(lse, dtype=np.float64) - rl).max()) if np.size(rl) else 0.0
+    log_parity(elements=int(go.size), bar_max=mx, plain_max=raw, mean=mean, lse_max=lerr)
+    assert np.isfinite(go).all(), "some outputs are not finite"
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean, raw)
+    if lerr is not None:
+        assert lerr <= lse_tol, lerr
 
 
 def dev_bf16(bits: np.ndarray, device="cuda") -> torch.Tensor:

@@ -299,6 +299,80 @@ def test_plan_rejects_bad_shapes(msa, field, value, status):
     assert e.value.status == status
 
 
+def _blocks_read(inst):
+    """Block-table entries a plan reads per sequence: logical blocks up to
+    the one holding the sequence's largest query position."""
+    out = []
+    for b in range(inst.num_seqs):
+        segs = inst.segments(b)
+        out.append(0 if not segs else (segs[-1][0] + segs[-1][1] - 1) // 16 + 1)
+    return out
+
+
+@pytest.mark.parametrize("case", PLAN_CASES)
+@pytest.mark.parametrize("tile_flag", [0, 16])
+def test_check_block_table_covers_every_entry_the_kernels_read(msa, case, tile_flag):
+    """The validator's range contains every block a work item (and an append
+    slice) touches, and holds exactly the entries the model above names."""
+    inst = workloads.make_random(keep_logical=False, **case)
+    plan = host_plan(msa, inst, kv_split_tokens=64, flags=tile_flag)
+    _, work, _ = msa.msa_plan_export(plan)
+    nread = _blocks_read(inst)
+    for w in work:
+        if w[3] > 0:
+            assert (int(w[5]) - 1) // 16 < nread[int(w[0])]
+    msa.msa_check_block_table(plan, inst.block_table)
+    rng = np.random.default_rng(case["seed"])
+    # a bad value at each read entry is found and named; unread entries are ignored
+    for b in range(inst.num_seqs):
+        for i in sorted(set(rng.integers(0, max(nread[b], 1), size=3).tolist())) if nread[b] else []:
+            for bad in (-1, inst.num_blocks, 2 ** 31 - 1):
+                bt = inst.block_table.copy()
+                bt[b, i] = bad
+                with pytest.raises(msa.MsaError) as e:
+                    msa.msa_check_block_table(plan, bt)
+                assert e.value.status == msa.MSA_ERR_INVALID_ARG
+                assert f"sequence {b}, logical block {i} maps to physical block {bad}" in msa.msa_last_error()
+        if nread[b] < inst.max_blocks_per_seq:
+            bt = inst.block_table.copy()
+            bt[b, nread[b]:] = -7
+            msa.msa_check_block_table(plan, bt)
+
+
+def test_check_block_table_reports_the_first_bad_entry(msa):
+    inst = workloads.make_layout(35, [100, 64, 300], [[(10, 5), (90, 10)], [], [(200, 1)]], 4, 2, 64,
+                                 keep_logical=False, permute_blocks=True)
+    plan = host_plan(msa, inst)
+    assert _blocks_read(inst) == [7, 0, 13]
+    bt = inst.block_table.copy()
+    bt[1, :] = -1            # sequence 1 has no query rows: nothing read
+    msa.msa_check_block_table(plan, bt)
+    bt[2, 12] = -3
+    bt[2, 4] = 10 ** 6
+    bt[0, 6] = -1
+    with pytest.raises(msa.MsaError):
+        msa.msa_check_block_table(plan, bt)
+    assert "sequence 0, logical block 6 maps to physical block -1" in msa.msa_last_error()
+    bt[0, 6] = 0
+    with pytest.raises(msa.MsaError):
+        msa.msa_check_block_table(plan, bt)
+    assert "sequence 2, logical block 4 maps to physical block 1000000" in msa.msa_last_error()
+
+
+def test_check_block_table_arguments(msa):
+    inst = workloads.make_config(1)
+    plan = host_plan(msa, inst)
+    lib = msa._lib
+    assert lib.msa_check_block_table(None, inst.block_table.ctypes.data, msa.MSA_TABLE_HOST, None) \
+        == msa.MSA_ERR_INVALID_ARG
+    assert lib.msa_check_block_table(plan.handle, None, msa.MSA_TABLE_HOST, None) == msa.MSA_ERR_INVALID_ARG
+    assert lib.msa_check_block_table(plan.handle, inst.block_table.ctypes.data, 7, None) \
+        == msa.MSA_ERR_INVALID_ARG
+    # a plan without query rows reads no entry: even a null table passes
+    empty = workloads.make_layout(36, [64], [[]], 4, 2, 64, keep_logical=False)
+    assert lib.msa_check_block_table(host_plan(msa, empty).handle, None, msa.MSA_TABLE_HOST, None) == msa.MSA_OK
+
+
 def test_plan_rejects_bad_options(msa):
     inst = workloads.make_layout(9, [256], [[(10, 30)]], 4, 2, 64)
     for kw in (dict(kv_split_tokens=100), dict(q_tile_tokens=65), dict(kv_split_tokens=-64)):

@@ -1,8 +1,9 @@
 """Parity of the HIP path (through the C ABI) with the CPU oracle on MI355X.
 
-Bar (bf16 inputs, bf16 output): max-abs <= 1e-2 (on the value before the
-output's own bf16 rounding, see ``tolerance.py``) and mean-abs <= 1e-3 over
-every compared element; lse within 2^-9 + 1e-4 (natural log); index handling
+Bar (bf16 inputs, bf16 output): max-abs <= 1e-2 (plain |stored - ref| where
+|ref| < 4; above, where half a bf16 spacing exceeds the bar, on the value
+before the output's own rounding, see ``tolerance.py``) and mean-abs <= 1e-3
+over every compared element; lse within 2^-9 + 1e-4 (natural log); index handling
 bit-exact (permuting physical blocks, poisoning blocks nobody references
 and garbage past the context end leave the output bit-identical).
 """
@@ -21,7 +22,7 @@ if not torch.cuda.is_available():  # collected on a CPU-only host with -m gpu
     pytest.skip("no GPU visible", allow_module_level=True)
 
 from gpu_helpers import (LSE_ABS, MAX_ABS, MEAN_ABS, DeviceInstance, bf16_to_f32,  # noqa: E402
-                         dev_bf16, errors, run)
+                         check_o, dev_bf16, errors, run)
 import paper_2606_02964_amd as msa  # noqa: E402
 
 
@@ -29,11 +30,7 @@ def check_full(inst, oracle_lib, **plan_kw):
     o, lse, plan = run(DeviceInstance(inst), **plan_kw)
     ro, rl = oracle_lib.forward(inst)
     go = bf16_to_f32(o)
-    assert np.isfinite(go).all(), "some output rows were not written"
-    mx, mean = errors(go, ro)
-    lerr = float(np.abs(lse.cpu().numpy().astype(np.float64) - rl).max())
-    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
-    assert lerr <= LSE_ABS, lerr
+    check_o(go, ro, lse.cpu().numpy(), rl)
     return go, lse.cpu().numpy(), plan
 
 
@@ -186,9 +183,7 @@ def test_scores_that_start_far_below_and_jump(oracle_lib, tile):
     o, lse, _ = run(DeviceInstance(inst), flags=tile)
     ro, rl = oracle_lib.forward(inst)
     go = bf16_to_f32(o)
-    assert np.isfinite(go).all()
-    mx, mean = errors(go, ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
+    check_o(go, ro)
     # the scores reach ~1200 before scaling: their fp32 accumulation over d
     # products adds up to d * 2^-24 * |q| |k| * scale to lse
     qn = float(np.linalg.norm(q, axis=-1).max())
@@ -197,18 +192,42 @@ def test_scores_that_start_far_below_and_jump(oracle_lib, tile):
     assert float(np.abs(lse.cpu().numpy().astype(np.float64) - rl).max()) <= bound
 
 
-@pytest.mark.parametrize("cfg,tile", [(2, 0), (3, 0), (4, 0), (5, 0), ("5-decode", 0),
-                                      (3, msa.MSA_PLAN_TILE_ROWS_32), (5, msa.MSA_PLAN_TILE_ROWS_32)])
-def test_named_workload_sampled_parity(oracle_lib, cfg, tile):
+# Oracle results of the last full-size workload, shared by the tests that run
+# it with different plans (one instance at a time: config 2 alone is 0.7 GB).
+_FULL = {}
+
+
+def _full_oracle(oracle_lib, cfg):
+    if cfg not in _FULL:
+        _FULL.clear()
+        inst = (workloads.make_config(5, decode_only=True) if cfg == "5-decode"
+                else workloads.make_config(cfg))
+        if cfg == 4:
+            # every row for one query head per KV head, a different head of
+            # each group: every work item of the plan is covered
+            G = inst.num_q_heads // inst.num_kv_heads
+            heads = np.array([g * G + g % G for g in range(inst.num_kv_heads)], dtype=np.int32)
+            rows = np.repeat(np.arange(inst.total_q, dtype=np.int64), heads.size)
+            hsel = np.tile(heads, inst.total_q)
+            ro, rl = oracle_lib.forward(inst, rows=rows, heads=hsel)
+            _FULL[cfg] = (inst, ro.reshape(inst.total_q, heads.size, -1),
+                          rl.reshape(inst.total_q, heads.size), heads)
+        else:
+            ro, rl = oracle_lib.forward(inst)
+            _FULL[cfg] = (inst, ro, rl, None)
+    return _FULL[cfg]
+
+
+@pytest.mark.parametrize("cfg,tile", [(2, 0), (3, 0), (3, msa.MSA_PLAN_TILE_ROWS_32), (4, 0),
+                                      (5, 0), (5, msa.MSA_PLAN_TILE_ROWS_32), ("5-decode", 0)])
+def test_named_workload_full_parity(oracle_lib, cfg, tile):
     """Full-size workloads in the benchmark's launch configuration (automatic
     plan; two of them also forced onto 32-row tiles, whose kernel then takes
-    prefill segments at full size): every output finite and inside the
-    convex hull of V, sampled
-    (row, head) items against the oracle."""
-    if cfg == "5-decode":
-        inst, cfg = workloads.make_config(5, decode_only=True), 6
-    else:
-        inst = workloads.make_config(cfg)
+    prefill segments at full size), compared with the oracle on every output
+    element and every lse; the long-context workload on every row for one
+    query head per KV head (a different head of each group).  Every output
+    is also finite and inside the convex hull of V."""
+    inst, ro, rl, heads = _full_oracle(oracle_lib, cfg)
     d = DeviceInstance(inst)
     o, lse, plan = run(d, flags=tile)
     if tile:
@@ -218,13 +237,10 @@ def test_named_workload_sampled_parity(oracle_lib, cfg, tile):
     assert torch.isfinite(lse).all().item()
     vmax = float(np.abs(workloads.bf16_bits_to_f32(inst.v_cache)).max())
     assert float(go.abs().max()) <= vmax * (1 + 2 ** -7)
-    rows, heads = _sample_items(inst, 1500, seed=cfg)
-    ro, rl = oracle_lib.forward(inst, rows=rows, heads=heads)
-    gsel = go[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
-    mx, mean = errors(gsel, ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
-    lsel = lse[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
-    assert float(np.abs(lsel - rl).max()) <= LSE_ABS
+    if heads is not None:
+        hs = torch.from_numpy(heads).long().cuda()
+        go, lse = go[:, hs], lse[:, hs]
+    check_o(go.cpu().numpy(), ro, lse.cpu().numpy(), rl)
 
 
 def test_longest_context_sampled_parity(oracle_lib):
@@ -247,10 +263,8 @@ def test_longest_context_sampled_parity(oracle_lib):
     heads = np.r_[heads, np.arange(edges.size, dtype=np.int32) * 3 % 8].astype(np.int32)
     ro, rl = oracle_lib.forward(inst, rows=rows, heads=heads)
     gsel = go[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
-    mx, mean = errors(gsel, ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
     lsel = lse[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
-    assert float(np.abs(lsel - rl).max()) <= LSE_ABS
+    check_o(gsel, ro, lsel, rl)
 
 
 def test_large_decode_batch_sampled_parity(oracle_lib):
@@ -272,10 +286,8 @@ def test_large_decode_batch_sampled_parity(oracle_lib):
     rows, heads = _sample_items(inst, 300, seed=43)
     ro, rl = oracle_lib.forward(inst, rows=rows, heads=heads)
     gsel = go[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
-    mx, mean = errors(gsel, ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
     lsel = lse[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
-    assert float(np.abs(lsel - rl).max()) <= LSE_ABS
+    check_o(gsel, ro, lsel, rl)
 
 
 def test_config4_forced_split_matches_unsplit(oracle_lib):
@@ -293,8 +305,7 @@ def test_config4_forced_split_matches_unsplit(oracle_lib):
     rows, heads = _sample_items(inst, 600, seed=44)
     ro, _ = oracle_lib.forward(inst, rows=rows, heads=heads)
     sel = o2.float()[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()]
-    mx, mean = errors(sel.cpu().numpy(), ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS
+    check_o(sel.cpu().numpy(), ro)
 
 
 @pytest.mark.parametrize("tile", [0, msa.MSA_PLAN_TILE_ROWS_32])
@@ -358,8 +369,7 @@ def test_strided_output_guard_rows_untouched(oracle_lib):
         mask[h * head_stride: h * head_stride + D] = False
     assert (rows[:, mask] == 7.0).all()
     ro, _ = oracle_lib.forward(inst)
-    mx, mean = errors(o, ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS
+    check_o(o, ro)
 
 
 def test_block_ids_past_2gib_offsets(oracle_lib):
@@ -389,8 +399,7 @@ def test_block_ids_past_2gib_offsets(oracle_lib):
     torch.cuda.synchronize()
     del k, v
     ro, _ = oracle_lib.forward(inst)
-    mx, mean = errors(bf16_to_f32(o), ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS
+    check_o(bf16_to_f32(o), ro)
 
 
 def test_forward_argument_errors():
@@ -433,8 +442,7 @@ def test_plan_reuse_across_layers_and_streams(oracle_lib):
     torch.cuda.synchronize()
     for o, ii in zip(outs, (inst, other)):
         ro, _ = oracle_lib.forward(ii)
-        mx, mean = errors(bf16_to_f32(o), ro)
-        assert mx <= MAX_ABS and mean <= MEAN_ABS
+        check_o(bf16_to_f32(o), ro)
 
 
 @pytest.mark.parametrize("hq,hkv,d,tile", [(64, 2, 128, 0), (64, 2, 64, msa.MSA_PLAN_TILE_ROWS_128),
@@ -495,3 +503,37 @@ def test_hip_graph_replays_match_eager(tile):
         assert torch.equal(o.view(torch.int16), o_ref.view(torch.int16)), rep
         assert torch.equal(lse.view(torch.int32), l_ref.view(torch.int32)), rep
         (d.q.float() * 2).sum().item()  # unrelated eager work between replays
+
+
+def test_check_block_table_on_device_tables():
+    """The debug validator on device-resident tables: a good table passes; a
+    corrupted copy (an entry the plan reads set past the cache, or to -1) is
+    reported with its sequence and logical block, on the default and on a
+    side stream.  msa_forward never sees the corrupted tables."""
+    inst = workloads.make_random(207, num_seqs=4, num_q_heads=8, num_kv_heads=2, head_dim=64,
+                                 min_len=100, max_len=600, max_segs=3, keep_logical=False)
+    d = DeviceInstance(inst)
+    plan = d.plan()
+    msa.msa_check_block_table(plan, d.bt)
+    # last logical block each sequence's rows read (-1: no rows)
+    last = [((lambda sg: (sg[-1][0] + sg[-1][1] - 1) // 16 if sg else -1)(inst.segments(b)))
+            for b in range(inst.num_seqs)]
+    with_rows = [b for b in range(inst.num_seqs) if last[b] >= 0]
+    assert len(with_rows) >= 2
+    b0, b1 = with_rows[0], with_rows[-1]
+    side = torch.cuda.Stream()
+    for b, blk, val, stream in ((b0, 0, inst.num_blocks, None), (b1, last[b1], -1, side),
+                                (b1, last[b1] // 2, 2 ** 31 - 1, None)):
+        bad = d.bt.clone()
+        bad[b, blk] = val
+        torch.cuda.synchronize()
+        with pytest.raises(msa.MsaError) as e:
+            msa.msa_check_block_table(plan, bad, stream=stream)
+        assert e.value.status == msa.MSA_ERR_INVALID_ARG
+        assert f"sequence {b}, logical block {blk} maps to physical block {val}" in msa.msa_last_error()
+    # entries past the last one read are ignored, and so are the rows of
+    # sequences without query rows
+    ok = d.bt.clone()
+    for b in range(inst.num_seqs):
+        ok[b, last[b] + 1:] = -1
+    msa.msa_check_block_table(plan, ok)

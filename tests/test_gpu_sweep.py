@@ -12,8 +12,9 @@ Each case draws its own shape and plan options:
 - forced key splits of 64-320 keys or none;
 - automatic, 128-row, 256-row or 32-row tiles.
 
-The bar is the same as the other parity tests (see ``tolerance.py`` for
-how the max-abs bar treats the output's own bf16 rounding).
+The bar is the same as the other parity tests: plain max-abs <= 1e-2 where
+the oracle's value is below 4 in magnitude (see ``tolerance.py`` for the
+reading above that), mean-abs <= 1e-3, lse within 2^-9 + 1e-4.
 """
 import numpy as np
 import pytest
@@ -26,8 +27,7 @@ pytestmark = pytest.mark.gpu
 if not torch.cuda.is_available():  # collected on a CPU-only host with -m gpu
     pytest.skip("no GPU visible", allow_module_level=True)
 
-from gpu_helpers import (LSE_ABS, MAX_ABS, MEAN_ABS, DeviceInstance, bf16_to_f32, errors,  # noqa: E402
-                         raw_max_abs, run)
+from gpu_helpers import DeviceInstance, bf16_to_f32, check_o, run  # noqa: E402
 import paper_2606_02964_amd as msa  # noqa: E402
 
 GROUPS = [1, 2, 3, 4, 5, 7, 8, 12, 16]
@@ -54,9 +54,4 @@ def test_random_shape_sweep(oracle_lib, seed):
     if inst.total_q == 0:
         return
     ro, rl = oracle_lib.forward(inst)
-    go = bf16_to_f32(o)
-    assert np.isfinite(go).all(), "some output rows were not written"
-    mx, mean = errors(go, ro)
-    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean, raw_max_abs(go, ro), plan.info())
-    lerr = float(np.abs(lse.cpu().numpy().astype(np.float64) - rl).max())
-    assert lerr <= LSE_ABS, lerr
+    check_o(bf16_to_f32(o), ro, lse.cpu().numpy(), rl)

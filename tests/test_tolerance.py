@@ -1,8 +1,9 @@
-"""The bf16-aware max-abs bar (CPU only): the distance from the oracle's
-value to the rounding interval of the stored bf16 number."""
+"""The max-abs bar (CPU only): plain |stored - ref| below |ref| = 4, and
+above it the distance from the oracle's value to the rounding interval of
+the stored bf16 number."""
 import numpy as np
 
-from tolerance import bf16_interval_distance, errors
+from tolerance import GRID_LIMIT, MAX_ABS, bar_errors, bf16_interval_distance, errors
 
 
 def _bf16(x):
@@ -42,12 +43,35 @@ def test_opposite_sign_and_zero():
     assert abs(d[1] - 0.25) < 1e-30 + 1e-12
 
 
-def test_errors_reports_interval_distance_and_plain_mean():
+def test_plain_bar_below_four():
+    """Sweep seed 141's row: the oracle is -2.4633527 and the kernel stored
+    -2.453125 (0.0102 away).  Below 4 the bar is the plain difference, so
+    that element fails, although the oracle lies only 0.0024 from the stored
+    number's rounding interval."""
     g = np.array([np.float32(-2.453125), np.float32(1.0)])
     ref = np.array([-2.4633527, 1.0])
     mx, mean = errors(g, ref)
-    assert abs(mx - (2.4633527 - 2.4609375)) < 1e-12
+    assert abs(mx - (2.4633527 - 2.453125)) < 1e-12 and mx > MAX_ABS
     assert abs(mean - (2.4633527 - 2.453125) / 2) < 1e-12
+
+
+def test_correct_rounding_always_meets_the_plain_bar_below_four():
+    rng = np.random.default_rng(1)
+    ref = rng.uniform(-GRID_LIMIT, GRID_LIMIT, 200000)
+    ref = ref[np.abs(ref) < GRID_LIMIT]
+    assert bar_errors(_bf16(ref), ref).max() <= 2.0 ** -8 * 2 + 1e-15
+
+
+def test_interval_reading_from_four_up():
+    # on [4, 8) the spacing is 2^-5: a correctly rounded value can sit
+    # 2^-6 = 0.0156 from the oracle, beyond a plain 1e-2
+    ref = np.array([4.0 + 2 ** -6 - 1e-9])
+    g = _bf16(ref)
+    assert abs(float(g[0]) - ref[0]) > MAX_ABS
+    assert bar_errors(g, ref)[0] == 0.0
+    # 1e-3 past the rounding interval counts as 1e-3
+    ref2 = np.array([-(5.0 + 2 ** -6 + 1e-3)])
+    assert abs(bar_errors(np.array([np.float32(-5.0)]), ref2)[0] - 1e-3) < 1e-12
 
 
 def test_rejects_values_off_the_bf16_grid():
