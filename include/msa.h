@@ -207,6 +207,31 @@ msa_status msa_forward(msa_plan_t plan, const void *q, const void *k_cache, cons
                        size_t workspace_bytes, void *hip_stream);
 
 /*
+ * msa_forward_noalloc: msa_forward for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the workspace is a scratch array of
+ * MSA_NOALLOC_WORKSPACE_BYTES inside the library, one per device, held
+ * until the process ends.  The call allocates and frees nothing.  Arguments
+ * and results are those of msa_forward without the workspace; the outputs
+ * are bit-identical to msa_forward's.
+ *
+ * Every call on a device shares that device's array and leaves it holding
+ * its partial results: calls that may overlap on one device (other streams,
+ * other threads) race and must be ordered by the caller.  The first call on
+ * each device looks the array's device address up (hipGetSymbolAddress,
+ * with that device current) and keeps it; make that first call before
+ * capturing a graph.
+ *
+ * Returns MSA_ERR_UNSUPPORTED, launching nothing, when the plan's workspace
+ * (msa_plan_info().workspace_bytes) exceeds MSA_NOALLOC_WORKSPACE_BYTES;
+ * otherwise the statuses of msa_forward.
+ */
+#define MSA_NOALLOC_WORKSPACE_BYTES (64ull << 20)
+msa_status msa_forward_noalloc(msa_plan_t plan, const void *q, const void *k_cache,
+                               const void *v_cache, const int32_t *block_table, void *o, float *lse,
+                               void *hip_stream);
+
+/*
  * msa_kv_append: write the fresh keys and values of every packed query row
  * into the paged cache, at the row's absolute position.  All segments'
  * tokens go through one forward pass (Sec. 4.1), so each layer produces K/V

@@ -7,7 +7,8 @@ fallback: importing this package without a built library raises.
 
 Functions carry the C names: ``msa_plan``, ``msa_plan_info``,
 ``msa_forward``, ``msa_kv_append``, ``msa_plan_destroy``,
-``msa_last_error``, ``msa_plan_export``, ``msa_check_block_table``.  Device buffers are passed as objects with a
+``msa_last_error``, ``msa_plan_export``, ``msa_check_block_table``,
+``msa_forward_noalloc``.  Device buffers are passed as objects with a
 ``data_ptr()`` method (e.g. torch tensors) or as integer addresses; streams
 as ``hipStream_t`` integers or objects with ``cuda_stream`` (torch streams).
 """
@@ -47,6 +48,7 @@ MSA_PLAN_TILE_ROWS_256 = 8
 MSA_PLAN_TILE_ROWS_32 = 16
 MSA_TABLE_HOST = 0
 MSA_TABLE_DEVICE = 1
+MSA_NOALLOC_WORKSPACE_BYTES = 64 << 20
 
 _i32, _i64, _f32, _f64, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 
@@ -91,6 +93,8 @@ _lib.msa_last_error.restype = ctypes.c_char_p
 _lib.msa_last_error.argtypes = []
 _lib.msa_plan_export.restype = _i32
 _lib.msa_plan_export.argtypes = [_P, _P, _P, _P]
+_lib.msa_forward_noalloc.restype = _i32
+_lib.msa_forward_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P]
 _lib.msa_check_block_table.restype = _i32
 _lib.msa_check_block_table.argtypes = [_P, _P, _i32, _P]
 
@@ -116,7 +120,7 @@ _lib.msa_evictor_replay.restype = _i32
 _lib.msa_evictor_replay.argtypes = [_P, _i64, _P, _P, _P, _P, _P, ctypes.POINTER(_i64)]
 
 EXPORTED = ("msa_plan", "msa_plan_info", "msa_forward", "msa_kv_append", "msa_plan_destroy",
-            "msa_last_error", "msa_plan_export", "msa_check_block_table",
+            "msa_last_error", "msa_plan_export", "msa_check_block_table", "msa_forward_noalloc",
             "msa_evictor_create", "msa_evictor_destroy", "msa_evictor_add", "msa_evictor_remove",
             "msa_evictor_evict", "msa_evictor_set_lambda", "msa_evictor_set_lifespan",
             "msa_evictor_size", "msa_evictor_log_weight", "msa_evictor_replay")
@@ -243,6 +247,14 @@ def msa_forward(plan: Plan, q, k_cache, v_cache, block_table, o, lse=None, works
     _check(_lib.msa_forward(plan.handle, _addr(q), _addr(k_cache), _addr(v_cache),
                             _addr(block_table), _addr(o), _addr(lse), _addr(workspace),
                             int(workspace_bytes), _stream(stream)))
+
+
+def msa_forward_noalloc(plan: Plan, q, k_cache, v_cache, block_table, o, lse=None,
+                        stream=None) -> None:
+    """msa_forward with the library's own scratch workspace (no allocation;
+    calls that overlap on one device race, see include/msa.h)."""
+    _check(_lib.msa_forward_noalloc(plan.handle, _addr(q), _addr(k_cache), _addr(v_cache),
+                                    _addr(block_table), _addr(o), _addr(lse), _stream(stream)))
 
 
 def msa_kv_append(plan: Plan, k_new, v_new, block_table, k_cache, v_cache,

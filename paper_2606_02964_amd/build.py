@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libmsa.so")
-SOURCES = ["plan.cpp", "api.cpp", "evictor.cpp", "attn.hip", "append.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "evictor.cpp", "attn.hip", "append.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 
