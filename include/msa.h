@@ -127,7 +127,7 @@ typedef struct msa_plan_opts {
 /* Figures describing a plan. */
 typedef struct msa_plan_info_t {
   int64_t total_q;          /* packed query rows */
-  int64_t num_work;         /* attention work items (workgroups launched, incl. padding) */
+  int64_t num_work;         /* attention work items (tiles x key ranges) */
   int64_t num_tiles;        /* query tiles x kv heads before key splitting */
   int64_t num_merge;        /* tiles whose keys were split (merge work items) */
   int64_t max_splits;       /* largest number of key splits of one tile */
@@ -137,6 +137,7 @@ typedef struct msa_plan_info_t {
   double planned_bytes;     /* Q + O + K/V bytes the executed tiles request */
   double min_bytes;         /* Q + O + K/V of visible keys once per (seq, kv head) */
   int64_t tile_rows;        /* rows per tile of this plan: 32, 128 or 256 */
+  int64_t num_workgroups;   /* workgroups launched; each runs its own list of work items */
 } msa_plan_info_t;
 
 /*
@@ -308,10 +309,11 @@ const char *msa_last_error(void);
  * inspection.  Any output pointer may be NULL.
  *   row_pos  [total_q] int32: absolute position of each packed row
  *   work     [num_work * 8] int32: per work item {seq, kv_head, row0, nrows,
- *            kv_lo, kv_hi, out_slot, flags}; rows row0 .. row0+nrows-1 of
+ *            kv_lo, kv_hi, out_slot, wg}; rows row0 .. row0+nrows-1 of
  *            sequence seq, keys [kv_lo, kv_hi); out_slot -1 writes the final
- *            output, else the workspace slot of a partial result; nrows == 0
- *            marks an empty padding item
+ *            output, else the workspace slot of a partial result; wg is the
+ *            workgroup that runs it (items of one workgroup are adjacent, in
+ *            run order, workgroups ascending; workgroup i runs on XCD i % 8)
  *   merge    [num_merge * 8] int32: per split tile {seq, kv_head, row0, nrows,
  *            nsplit, slot0, 0, 0}: slots slot0 .. slot0+nsplit-1 in key order
  */

@@ -72,7 +72,7 @@ class msa_plan_info_t(ctypes.Structure):
     _fields_ = [("total_q", _i64), ("num_work", _i64), ("num_tiles", _i64), ("num_merge", _i64),
                 ("max_splits", _i64), ("workspace_bytes", _i64), ("useful_flops", _f64),
                 ("tile_flops", _f64), ("planned_bytes", _f64), ("min_bytes", _f64),
-                ("tile_rows", _i64)]
+                ("tile_rows", _i64), ("num_workgroups", _i64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -20,9 +20,10 @@ struct msa_plan_s {
   bool host_only = true;
   int device = -1;
   std::vector<char> staging;  // host image of the device buffer (kept alive for the async copy)
-  char* dev = nullptr;        // device buffer: row_pos | work | merge | append
+  char* dev = nullptr;        // device buffer: row_pos | work | merge | append | wg_ptr
   const int32_t* d_row_pos = nullptr;
   const msa::WorkItem* d_work = nullptr;
+  const int32_t* d_wg_ptr = nullptr;
   const msa::MergeItem* d_merge = nullptr;
   const msa::AppendItem* d_append = nullptr;
 };
@@ -76,6 +77,7 @@ msa_status msa::forward_impl(const char* who, msa_plan_t plan, const void* q, co
   p.block_table = block_table;
   p.row_pos = plan->d_row_pos;
   p.work = plan->d_work;
+  p.wg_ptr = plan->d_wg_ptr;
   p.o = static_cast<uint16_t*>(o);
   p.lse = lse;
   p.ws = static_cast<float*>(workspace);
@@ -94,7 +96,8 @@ msa_status msa::forward_impl(const char* who, msa_plan_t plan, const void* q, co
   p.group = hp.group;
   p.tile_tokens = hp.tile_tokens;
   p.scale_log2 = s.scale * 1.4426950408889634f;
-  int rc = msa::launch_attn(p, s.head_dim, hp.tile_rows, (int)hp.work.size(), hip_stream);
+  const int num_wg = hp.wg_ptr.empty() ? 0 : (int)hp.wg_ptr.size() - 1;
+  int rc = msa::launch_attn(p, s.head_dim, hp.tile_rows, num_wg, hip_stream);
   if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string(w + ": attention launch failed: ") +
                                                     hipGetErrorString((hipError_t)rc));
   if (!hp.merge.empty()) {
@@ -147,10 +150,12 @@ msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int
     const size_t n_work = hp.work.size() * sizeof(msa::WorkItem);
     const size_t n_merge = hp.merge.size() * sizeof(msa::MergeItem);
     const size_t n_append = hp.append.size() * sizeof(msa::AppendItem);
+    const size_t n_wg = hp.wg_ptr.size() * sizeof(int32_t);
     const size_t off_work = align_up(n_row, 256);
     const size_t off_merge = off_work + align_up(n_work, 256);
     const size_t off_append = off_merge + align_up(n_merge, 256);
-    const size_t bytes = std::max<size_t>(off_append + n_append, 256);
+    const size_t off_wg = off_append + align_up(n_append, 256);
+    const size_t bytes = std::max<size_t>(off_wg + n_wg, 256);
     try {
       plan->staging.assign(bytes, 0);
     } catch (const std::bad_alloc&) {
@@ -161,6 +166,7 @@ msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int
     if (n_work) std::memcpy(plan->staging.data() + off_work, hp.work.data(), n_work);
     if (n_merge) std::memcpy(plan->staging.data() + off_merge, hp.merge.data(), n_merge);
     if (n_append) std::memcpy(plan->staging.data() + off_append, hp.append.data(), n_append);
+    if (n_wg) std::memcpy(plan->staging.data() + off_wg, hp.wg_ptr.data(), n_wg);
     const hipError_t gd = hipGetDevice(&plan->device);
     if (gd != hipSuccess) {
       delete plan;
@@ -183,6 +189,7 @@ msa_status msa_plan(const msa_shape* shape, const int32_t* seq_kv_len, const int
     plan->d_row_pos = reinterpret_cast<const int32_t*>(plan->dev);
     plan->d_work = reinterpret_cast<const msa::WorkItem*>(plan->dev + off_work);
     plan->d_merge = reinterpret_cast<const msa::MergeItem*>(plan->dev + off_merge);
+    plan->d_wg_ptr = reinterpret_cast<const int32_t*>(plan->dev + off_wg);
     plan->d_append = reinterpret_cast<const msa::AppendItem*>(plan->dev + off_append);
   }
   *out = plan;
@@ -203,6 +210,7 @@ msa_status msa_plan_info(msa_plan_t plan, msa_plan_info_t* info) {
   info->planned_bytes = hp.planned_bytes;
   info->min_bytes = hp.min_bytes;
   info->tile_rows = hp.tile_rows;
+  info->num_workgroups = hp.wg_ptr.empty() ? 0 : (int64_t)hp.wg_ptr.size() - 1;
   return MSA_OK;
 }
 

@@ -4,12 +4,13 @@
 // per wave) per work item: query rows of one sequence sharing one KV head,
 // over one key range.  Each 64-key step:
 //   - paged gather: the step's 4 cache blocks are looked up in the block
-//     table (scalar loads) and copied straight into LDS (global_load_lds,
+//     table (ids preloaded one lane per step, read with v_readlane) and
+//     copied straight into LDS (global_load_lds,
 //     16 bytes a lane, no staging registers): K as [key][d] rows, V as the
 //     cache's channel-major [d][16 keys] pages, 16-byte chunks XOR-swizzled
 //     so that every operand read is free of bank conflicts.  K runs one step
-//     ahead of V in rings of two stages.  The block-id loads and the copies
-//     are inline assembly (see sload_i32 and dma16 for why);
+//     ahead of V in rings of two stages.  The copies are inline assembly
+//     (see dma16 for why);
 //   - S^T = K Q^T on v_mfma_f32_32x32x16_bf16.  K is the A operand, so each
 //     lane holds one query row (a column of S^T) and 16 of the 32 keys: the
 //     row max and row sum need one exchange with the lane 32 apart only;
@@ -21,8 +22,8 @@
 //     FMA per score against a reference max that only moves (and O is only
 //     rescaled) when a row's max grows by more than 2^8.  The row max itself
 //     is only taken when a step's weights may have outgrown the reference
-//     (see settle); the row sum adds the bf16-rounded weights with v_dot2
-//     against (1, 1);
+//     (see settle); the row sum adds the fp32 weights with plain adds (a
+//     v_dot2 of the packed weights stalls the MFMA stream on gfx950);
 //   - O^T += V^T P^T on the same MFMA, P packed to bf16 straight from the
 //     score registers.  The A-operand row order of K is permuted (bits 2 and 3
 //     of the row index swapped) so that the 8 scores a lane feeds to one PV
@@ -124,15 +125,6 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// scalar load of one wave-uniform int32 (through the scalar cache, waited
-// for at once); the compiler only emits vector loads here because the
-// global->LDS copies count as possible writes to global memory
-__device__ __forceinline__ int32_t sload_i32(const int32_t* a) {
-  int32_t v;
-  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(a) : "memory");
-  return v;
-}
-
 // running-max threshold of the lazy rescale: the reference max only moves
 // when a row's max grows by more than this (log2 units), so the unnormalised
 // weights stay <= 2^8
@@ -140,17 +132,20 @@ constexpr float kRescaleLog2 = 8.0f;
 // a lane's step sum of weights at which the row max is taken (see settle)
 constexpr float kSettleSum = 128.0f;
 
+// One work item of msa_attn.  smem: the K ring (2 steps) then the V ring
+// (2 steps).  Every wave leaves through the barrier that ends the item's
+// last step before its epilogue (registers only), so the next item may
+// refill the rings at once.
 template <int D, int W>
-__global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
+__device__ __forceinline__ void attn_item(const AttnParams& p, const WorkItem w, char* smem) {
   using T = Tile<D>;
   constexpr int kRows = 32 * W;  // tile rows
-  // K ring (2 steps) then V ring (2 steps); K runs one step ahead of V
-  __shared__ __attribute__((aligned(1024))) char smem[2 * T::kBytesK + 2 * T::kBytesV];
+  if (w.nrows == 0) return;  // (uniform over the workgroup)
 
-  const WorkItem w = p.work[blockIdx.x];
-  if (w.nrows == 0) return;  // padding item (uniform over the workgroup)
-
-  const int tid = threadIdx.x;
+  // lane-dependent set-up is computed per item (an opaque copy of the
+  // thread id keeps it from being hoisted and held across items)
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
   const int G = p.group;
@@ -213,14 +208,35 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   };
   const int n = (w.kv_hi - w.kv_lo + kKvStep - 1) / kKvStep;
   // A step has 8 pages: the K and the V page of each of its 4 blocks (page
-  // pg: block pg & 3, V if pg >= 4); wave w copies pages w, w + W, ...
-  // issue(sk, sv) copies the K pages of step sk and the V pages of step sv
-  // (-1: none).  All block ids are read (scalar loads) before the first
-  // copy, so no id load waits behind copies.  A block at or past kv_hi is not
+  // pg: block pg & 3, V if pg >= 4); wave w copies pages w, w + W, ..., all
+  // of block slot w & 3.  issue(sk, sv) copies the K pages of step sk and
+  // the V pages of step sv (-1: none).  A block at or past kv_hi is not
   // read; its V page is zero-filled instead (its K page keeps old values:
   // those keys are masked by selection, so never meet arithmetic).
+  // The block ids a wave needs sit in two registers, one lane per step:
+  // lane i of idv0 holds the id of block slot w & 3 of step id_base + i, of
+  // idv1 that of step id_base + 64 + i.  A step reads its id with
+  // v_readlane (no memory access); every 64 steps the window moves on and
+  // the next 64 ids load, 64 steps before they are needed.
   constexpr int kPagesPerWave = 8 / W;
+  const int bslot = wave & 3;
+  auto load_ids = [&](int s0) -> int32_t {
+    const int st = s0 + lane;
+    const int kb = w.kv_lo + st * kKvStep + bslot * kBlockSize;
+    return (st < n && kb < w.kv_hi) ? bt[kb >> 4] : 0;
+  };
+  int id_base = 0;
+  int32_t idv0 = load_ids(0), idv1 = load_ids(64);
+  auto step_id = [&](int st) -> int64_t {  // id_base <= st < id_base + 128 (wave-uniform)
+    const int i = st - id_base;
+    return i < 64 ? __builtin_amdgcn_readlane(idv0, i) : __builtin_amdgcn_readlane(idv1, i - 64);
+  };
   auto issue = [&](int sk, int sv) {
+    if (sk >= id_base + 128) {  // move the window on (uniform; once per 64 steps)
+      idv0 = idv1;
+      idv1 = load_ids(id_base + 128);
+      id_base += 64;
+    }
     int64_t ids[kPagesPerWave];
     bool have[kPagesPerWave], zero[kPagesPerWave];
 #pragma unroll
@@ -232,8 +248,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
       const int kb = w.kv_lo + st * kKvStep;
       have[k] = live && kb + bi * kBlockSize < w.kv_hi;
       zero[k] = live && !have[k] && pg >= 4;
-      ids[k] = 0;
-      if (have[k]) ids[k] = (int64_t)sload_i32(bt + (kb >> 4) + bi);
+      ids[k] = have[k] ? step_id(st) : 0;
     }
 #pragma unroll
     for (int k = 0; k < kPagesPerWave; ++k) {
@@ -319,24 +334,26 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
       sbuf[b][e >> 4][e & 15] = ((e >> 4) * 32 + ((e & 15) >> 3) * 16 + (e & 7)) <= lim ? x : -__builtin_inff();
     }
   };
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   // weights of the scores in sbuf[b] against the reference max, packed to
-  // bf16; ls gets their sum (the row sum adds the same bf16-rounded weights
-  // that enter the PV product, so the normalised weights sum to one exactly)
+  // bf16; ls gets the fp32 sum of the unrounded weights.  (The sum is taken
+  // with plain adds: a v_dot2 of the packed weights against (1, 1) would be
+  // one instruction per pair, but on gfx950 every dot2 stalls the matrix
+  // core's MFMA stream for many cycles, while adds issue beside it.)
   auto weights_plain = [&](int b, uint32_t (&pk)[16], float& ls) {
     const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
     ls = 0.0f;
 #pragma unroll
     for (int e = 0; e < 32; e += 2) {
-      pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][e >> 4][e & 15], c, nm)),
-                               __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][(e + 1) >> 4][(e + 1) & 15], c, nm)));
-      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
+      const float w0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][e >> 4][e & 15], c, nm));
+      const float w1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][(e + 1) >> 4][(e + 1) & 15], c, nm));
+      pk[e >> 1] = pack_bf16x2(w0, w1);
+      ls += w0 + w1;
     }
   };
   // On the step that holds a row's own position (its diagonal step) the
   // row's weights are carried as two bf16 terms: once the reference max is
-  // settled, w replaces each score in sbuf[b], the row sum is their fp32
-  // sum, and the PV product runs on hi = bf16(w) and on lo = bf16(w - hi)
+  // settled, w replaces each score in sbuf[b] and the PV product runs on
+  // hi = bf16(w) and on lo = bf16(w - hi)
   // (w - hi is exact in fp32), so hi + lo is within 2^-18 of w.  The
   // diagonal step holds a row's latest keys, and a row near the start of
   // the sequence has all its keys there: few keys then carry all the
@@ -344,15 +361,11 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   // about 2^-9 |v_i - v_j|.  Which steps do this depends on the row's own
   // position only (not on the rows sharing its wave), so a row's result
   // does not depend on its tile.
-  auto weights_inplace = [&](int b, float& ls) {
+  auto weights_inplace = [&](int b) {
     const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
-    ls = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 32; ++e) {
-      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][e >> 4][e & 15], c, nm));
-      sbuf[b][e >> 4][e & 15] = x;
-      ls += x;
-    }
+    for (int e = 0; e < 32; ++e)
+      sbuf[b][e >> 4][e & 15] = __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[b][e >> 4][e & 15], c, nm));
   };
   // packed bf16 lo terms of the weights e, e+1 held in sbuf[b], given their
   // hi terms (zero for a row off its diagonal step: own = false)
@@ -423,9 +436,10 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
 #pragma unroll
       for (int u = 0; u < kElPerQk; u += 2) {
         const int e = i * kElPerQk + u;
-        pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][e >> 4][e & 15], c, nm)),
-                                 __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][(e + 1) >> 4][(e + 1) & 15], c, nm)));
-        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
+        const float w0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][e >> 4][e & 15], c, nm));
+        const float w1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sbuf[B][(e + 1) >> 4][(e + 1) & 15], c, nm));
+        pk[e >> 1] = pack_bf16x2(w0, w1);
+        ls += w0 + w1;
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -509,11 +523,7 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
     settle(0, ls, [&]() { weights_plain(0, pk, ls); });
     const int s_lo = w.kv_lo + jj * kKvStep;
     const bool own = pos >= s_lo && pos < s_lo + kKvStep;  // this is the row's diagonal step
-    if (split) {  // the same weights in fp32, in place; hi(w) == pk
-      float lw;
-      weights_inplace(0, lw);
-      ls = own ? lw : ls;
-    }
+    if (split) weights_inplace(0);  // the same weights in fp32, in place; hi(w) == pk
     l_run += ls;
 #pragma unroll
     for (int i = 0; i < kPv; ++i) {
@@ -578,6 +588,16 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   }
 }
 
+// Persistent launch: workgroup i runs the items wg_ptr[i] .. wg_ptr[i+1]-1.
+template <int D, int W>
+__global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
+  using T = Tile<D>;
+  // K ring (2 steps) then V ring (2 steps); K runs one step ahead of V
+  __shared__ __attribute__((aligned(1024))) char smem[2 * T::kBytesK + 2 * T::kBytesV];
+  const int end = p.wg_ptr[blockIdx.x + 1];
+  for (int it = p.wg_ptr[blockIdx.x]; it < end; ++it) attn_item<D, W>(p, p.work[it], smem);
+}
+
 // msa_decode: tiles of up to 32 rows (decode-like plans).  Every wave of the
 // 4-wave workgroup holds the same 32 rows; wave w takes the 32-key
 // half-steps w, w + 4, w + 8, ... of the item's key range and reads their K
@@ -590,16 +610,27 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
 // with K's rows permuted (bits 2 and 3 swapped), the lazy reference max and
 // bf16 weights whose row sum uses the same rounded values.
 template <int D>
-__global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
-  constexpr int kWaves = 4, kHalf = 32;
-  constexpr int kOPad = D + 4;  // LDS row stride of the partial O (bank spread)
-  __shared__ __attribute__((aligned(16))) float mo[kWaves][32][kOPad];
-  __shared__ float mm[kWaves][32], ml[kWaves][32];
+struct DecodeLds {
+  static constexpr int kWaves = 4;
+  static constexpr int kOPad = D + 4;  // row stride of the partial O (bank spread)
+  float mo[kWaves][32][kOPad];
+  float mm[kWaves][32], ml[kWaves][32];
+};
 
-  const WorkItem w = p.work[blockIdx.x];
-  if (w.nrows == 0) return;  // padding item (uniform over the workgroup)
+// One work item of msa_decode; the LDS merge area is reused by the next item
+// only after the barrier the caller places between items.
+template <int D>
+__device__ __forceinline__ void decode_item(const AttnParams& p, const WorkItem w, DecodeLds<D>& lds) {
+  constexpr int kWaves = DecodeLds<D>::kWaves, kHalf = 32;
+  auto& mo = lds.mo;
+  auto& mm = lds.mm;
+  auto& ml = lds.ml;
+  if (w.nrows == 0) return;  // (uniform over the workgroup)
 
-  const int tid = threadIdx.x;
+  // lane-dependent set-up is computed per item (an opaque copy of the
+  // thread id keeps it from being hoisted and held across items)
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
   const int G = p.group;
@@ -692,7 +723,6 @@ __global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
   };
 
   const float c = p.scale_log2;
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float m_ref = -__builtin_inff(), l_run = 0.0f;
   f32x16 oacc[D / 32];
 #pragma unroll
@@ -726,9 +756,10 @@ __global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
       ls = 0.0f;
 #pragma unroll
       for (int e = 0; e < 16; e += 2) {
-        pk[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm)),
-                                 __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e + 1], c, nm)));
-        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[e >> 1]), ones, ls, false);
+        const float w0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm));
+        const float w1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e + 1], c, nm));
+        pk[e >> 1] = pack_bf16x2(w0, w1);
+        ls += w0 + w1;  // fp32 sum (no v_dot2: it stalls the MFMA stream)
       }
     };
     weights();
@@ -751,13 +782,8 @@ __global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
     const bool own = pos >= k0 && pos < k0 + kHalf;  // the row's diagonal half-step
     if (split) {  // the same weights in fp32, in place of the scores; hi(w) == pk
       const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
-      float lw = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        sc[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm));
-        lw += sc[e];
-      }
-      ls = own ? lw : ls;
+      for (int e = 0; e < 16; ++e) sc[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm));
     }
     l_run += ls;
 #pragma unroll
@@ -851,6 +877,16 @@ __global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
 }
 
 template <int D>
+__global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
+  __shared__ __attribute__((aligned(16))) DecodeLds<D> lds;
+  const int end = p.wg_ptr[blockIdx.x + 1];
+  for (int it = p.wg_ptr[blockIdx.x]; it < end; ++it) {
+    if (it > p.wg_ptr[blockIdx.x]) __syncthreads();  // the previous item's merge reads are done
+    decode_item<D>(p, p.work[it], lds);
+  }
+}
+
+template <int D>
 __global__ __launch_bounds__(256) void msa_merge_kernel(MergeParams p) {
   constexpr int kThreadsPerRow = D / 4;
   constexpr int kRowsPerPass = 256 / kThreadsPerRow;
@@ -887,21 +923,21 @@ __global__ __launch_bounds__(256) void msa_merge_kernel(MergeParams p) {
 
 }  // namespace
 
-int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_work, void* stream) {
+int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_wg, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (num_work <= 0) return 0;
+  if (num_wg <= 0) return 0;
   if (head_dim == 128 && tile_rows == kTileRowsNarrow)
-    hipLaunchKernelGGL((msa_attn_kernel<128, 4>), dim3(num_work), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((msa_attn_kernel<128, 4>), dim3(num_wg), dim3(256), 0, s, p);
   else if (head_dim == 128 && tile_rows == kTileRowsWide)
-    hipLaunchKernelGGL((msa_attn_kernel<128, 8>), dim3(num_work), dim3(512), 0, s, p);
+    hipLaunchKernelGGL((msa_attn_kernel<128, 8>), dim3(num_wg), dim3(512), 0, s, p);
   else if (head_dim == 64 && tile_rows == kTileRowsNarrow)
-    hipLaunchKernelGGL((msa_attn_kernel<64, 4>), dim3(num_work), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((msa_attn_kernel<64, 4>), dim3(num_wg), dim3(256), 0, s, p);
   else if (head_dim == 64 && tile_rows == kTileRowsWide)
-    hipLaunchKernelGGL((msa_attn_kernel<64, 8>), dim3(num_work), dim3(512), 0, s, p);
+    hipLaunchKernelGGL((msa_attn_kernel<64, 8>), dim3(num_wg), dim3(512), 0, s, p);
   else if (head_dim == 128 && tile_rows == kTileRowsDecode)
-    hipLaunchKernelGGL(msa_decode_kernel<128>, dim3(num_work), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(msa_decode_kernel<128>, dim3(num_wg), dim3(256), 0, s, p);
   else if (head_dim == 64 && tile_rows == kTileRowsDecode)
-    hipLaunchKernelGGL(msa_decode_kernel<64>, dim3(num_work), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(msa_decode_kernel<64>, dim3(num_wg), dim3(256), 0, s, p);
   else
     return (int)hipErrorInvalidValue;
   return (int)hipGetLastError();

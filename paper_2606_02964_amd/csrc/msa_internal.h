@@ -1,8 +1,9 @@
 // msa_internal.h -- tables shared by the host planner and the gfx950 kernels.
 //
-// A work item is one workgroup: up to tile_rows query rows of one sequence
+// A work item is one tile: up to tile_rows query rows of one sequence
 // that share one KV head (tokens x the G = Hq/Hkv query heads of the group,
 // row r <-> token r / G, head r % G) and one contiguous key range.  The
+// launch is persistent: each workgroup runs its own list of items.  The
 // planner packs consecutive query tokens of a sequence into a tile even
 // across segment gaps; each row keeps its own causal limit (its absolute
 // position), which is what the paper's per-token "equivalent seq_len" array
@@ -32,7 +33,7 @@ struct WorkItem {
   int32_t kv_lo;     // first key (multiple of kKvStep)
   int32_t kv_hi;     // one past the last key
   int32_t out_slot;  // -1: final output; >= 0: workspace slot of a partial
-  int32_t flags;     // reserved (0)
+  int32_t wg;        // the workgroup (blockIdx.x) that runs it
 };
 static_assert(sizeof(WorkItem) == 32, "WorkItem is exported as 8 int32");
 
@@ -59,6 +60,7 @@ struct AttnParams {
   const int32_t* block_table;
   const int32_t* row_pos;
   const WorkItem* work;
+  const int32_t* wg_ptr;  // workgroup i runs items wg_ptr[i] .. wg_ptr[i+1]-1, in order
   uint16_t* o;
   float* lse;        // may be null
   float* ws;         // workspace (partials), may be null when unused
@@ -84,7 +86,7 @@ struct MergeParams {
 };
 
 // Launchers (attn.hip).  Return a hipError_t value as int.
-int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_work, void* stream);
+int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_wg, void* stream);
 int launch_merge(const MergeParams& p, int head_dim, int num_merge, void* stream);
 
 }  // namespace msa

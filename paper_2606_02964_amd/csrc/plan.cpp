@@ -26,7 +26,10 @@
 //      i runs on XCD i % 8) so tiles sharing K/V share one XCD's L2.  Inside
 //      each XCD, groups start in decreasing order of their longest piece and
 //      a group's pieces run back to back, longest first, so that no long
-//      piece (a decode row over a long context) is left for the end.
+//      piece (a decode row over a long context) is left for the end;
+//   6. workgroups: the launch is persistent, one workgroup per slot, each
+//      with its own list of items; each XCD's queue is dealt out in order to
+//      the least-loaded workgroup of that XCD.
 #include "plan.h"
 
 #include <algorithm>
@@ -370,16 +373,34 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
     }
     queue[(size_t)x].push_back(pi);
   }
-  // Inside each XCD: groups by decreasing longest piece, then by id; pieces
-  // of one group stay adjacent, longest first.  Ordering by total group cost
-  // alone would leave a light group's long piece to run last.
+  // 6. workgroups: one persistent workgroup per slot (256 for 256-row
+  // tiles, one per CU; 512 otherwise, two per CU), or 8 per round of the
+  // XCD queues when that is fewer.  Workgroup i runs on XCD i % 8 and works
+  // through its own list of items, so no workgroup waits for a dispatch
+  // between items.  Each XCD's pieces go, in queue order (below), to the
+  // least-loaded workgroup of that XCD (cost: key steps plus one for the
+  // per-item start-up), as a dynamic dispatch would hand them out; a
+  // workgroup runs its list in that order.  A plan with at most one piece
+  // per workgroup gets one each.
+  size_t rounds = 0;
+  for (const auto& q : queue) rounds = std::max(rounds, q.size());
+  const int64_t nwg = std::min<int64_t>(slots_total, (int64_t)rounds * kXcds);
+  std::vector<std::vector<int32_t>> wg_list((size_t)nwg);
+  std::vector<double> wg_load((size_t)nwg, 0.0);
+  // Inside each XCD the queue runs groups by decreasing longest piece (then
+  // by id), a group's pieces adjacent and longest first, so that the
+  // workgroups of an XCD work on the same groups at the same time and share
+  // their K/V in that XCD's L2; ordering by total group cost alone would
+  // leave a light group's long piece (a decode row over a long context) to
+  // run last.
   std::vector<double> gmax((size_t)ngroups, 0.0);
   for (const Piece& p : pieces) {
     const Unit& u = units[(size_t)p.unit];
     double& m = gmax[(size_t)((int64_t)u.seq * Hkv + u.kv_head)];
     m = std::max(m, pcost(p));
   }
-  for (auto& qx : queue)
+  for (int x = 0; x < kXcds; ++x) {
+    auto& qx = queue[(size_t)x];
     std::stable_sort(qx.begin(), qx.end(), [&](int32_t a, int32_t b) {
       const Piece& pa = pieces[(size_t)a];
       const Piece& pb = pieces[(size_t)b];
@@ -390,22 +411,27 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
       if (ga != gb) return ga < gb;
       return pcost(pa) > pcost(pb);
     });
-  size_t rounds = 0;
-  for (const auto& q : queue) rounds = std::max(rounds, q.size());
-  // trim trailing XCDs with nothing in the last round so a small problem
-  // does not launch a whole row of padding
-  P.work.reserve(rounds * kXcds);
-  for (size_t k = 0; k < rounds; ++k)
-    for (int x = 0; x < kXcds; ++x) {
-      if (k < queue[(size_t)x].size()) {
-        const Piece& p = pieces[(size_t)queue[(size_t)x][k]];
-        const Unit& u = units[(size_t)p.unit];
-        P.work.push_back(WorkItem{u.seq, u.kv_head, u.row0, u.nrows, p.lo, p.hi, p.slot, 0});
-      } else {
-        P.work.push_back(WorkItem{0, 0, 0, 0, 0, 0, -1, 0});
-      }
+    for (int32_t pi : qx) {
+      int64_t best = -1;
+      for (int64_t wgi = x; wgi < nwg; wgi += kXcds)
+        if (best < 0 || wg_load[(size_t)wgi] < wg_load[(size_t)best]) best = wgi;
+      wg_list[(size_t)best].push_back(pi);
+      wg_load[(size_t)best] += pcost(pieces[(size_t)pi]);
     }
-  while (!P.work.empty() && P.work.back().nrows == 0) P.work.pop_back();
+  }
+  // trailing workgroups with nothing to do are not launched
+  int64_t launched = nwg;
+  while (launched > 0 && wg_list[(size_t)launched - 1].empty()) --launched;
+  P.wg_ptr.assign(1, 0);
+  P.work.reserve(pieces.size());
+  for (int64_t wgi = 0; wgi < launched; ++wgi) {
+    for (int32_t pi : wg_list[(size_t)wgi]) {
+      const Piece& p = pieces[(size_t)pi];
+      const Unit& u = units[(size_t)p.unit];
+      P.work.push_back(WorkItem{u.seq, u.kv_head, u.row0, u.nrows, p.lo, p.hi, p.slot, (int32_t)wgi});
+    }
+    P.wg_ptr.push_back((int32_t)P.work.size());
+  }
 
   // figures
   const double hq = s.num_q_heads;

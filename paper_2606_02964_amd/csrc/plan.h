@@ -18,7 +18,8 @@ struct HostPlan {
   int64_t total_q = 0;
   std::vector<int32_t> row_pos;   // [total_q] absolute position of each packed row
   std::vector<int32_t> seq_blocks; // [num_seqs] block-table entries the plan reads per sequence
-  std::vector<WorkItem> work;     // launch order (blockIdx.x)
+  std::vector<WorkItem> work;     // items grouped by workgroup (workgroup i: wg_ptr[i] .. wg_ptr[i+1]-1)
+  std::vector<int32_t> wg_ptr;    // [num_workgroups + 1]; workgroup i runs on XCD i % 8
   std::vector<MergeItem> merge;
   std::vector<AppendItem> append; // one per (segment, cache block) slice
   int64_t num_tiles = 0;          // tiles x kv heads before splitting

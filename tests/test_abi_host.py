@@ -495,41 +495,59 @@ def test_fused_ablation_layouts():
                 assert suf[0] == (0, ctx - 128 - cached)
 
 
-def _xcd_queues(work):
-    """Work item i runs on XCD i % 8: per XCD, the (group, keys) of its items
-    in launch order (padding items skipped)."""
-    queues = [[] for _ in range(8)]
-    for i, w in enumerate(work):
-        if int(w[3]) > 0:
-            queues[i % 8].append(((int(w[0]), int(w[1])), (int(w[5]) - int(w[4]) + 63) // 64))
-    return queues
+def check_workgroups(work, info, num_kv_heads):
+    """The persistent launch: items grouped by workgroup (adjacent, ascending),
+    workgroup i on XCD i % 8; inside a workgroup items run in XCD-queue
+    order (groups by decreasing longest piece, then id; a group's pieces by
+    decreasing cost, cost = key steps + 1); per XCD the workgroups' loads
+    differ by at most the largest item cost of that XCD (greedy
+    least-loaded assignment); a (sequence, KV head) group's items share one
+    XCD unless the group alone is more than half of an XCD's share."""
+    wg = work[:, 7].astype(np.int64)
+    nwg = info["num_workgroups"]
+    slots = 256 if info["tile_rows"] == 256 else 512
+    assert 0 < nwg <= slots and (np.diff(wg) >= 0).all() and wg.min() >= 0 and wg.max() == nwg - 1
+    cost = (work[:, 5] - work[:, 4] + 63) // 64 + 1
+    groups = work[:, 0].astype(np.int64) * num_kv_heads + work[:, 1]
+    gmax = {g: cost[groups == g].max() for g in np.unique(groups)}
+    key = [(-gmax[g], g, -c) for g, c in zip(groups, cost)]
+    for w in np.unique(wg):
+        k = [key[i] for i in np.where(wg == w)[0]]
+        assert all(a <= b for a, b in zip(k, k[1:])), "a workgroup's items are out of queue order"
+    load = np.bincount(wg, weights=cost, minlength=nwg)
+    for x in range(8):
+        mine = np.arange(x, nwg, 8)
+        if mine.size == 0:
+            continue
+        on_x = (wg % 8) == x
+        if on_x.any():
+            assert load[mine].max() - load[mine].min() <= cost[on_x].max()
+    total = cost.sum()
+    for gr in np.unique(groups):
+        sel = groups == gr
+        if cost[sel].sum() <= 0.5 * total / 8:
+            assert len(np.unique(wg[sel] % 8)) == 1, "a group's items are spread over XCDs"
+    if len(work) <= nwg:
+        assert len(np.unique(wg)) == len(work), "one item per workgroup when they fit"
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 5])
-def test_xcd_queue_order(msa, cfg):
-    """Inside each XCD queue, (sequence, KV head) groups start in decreasing
-    order of their longest piece, a group's pieces are adjacent and run
-    longest first.  On the mixed workload this puts the decode rows over the
-    longest contexts ahead of the prefill groups with shorter pieces."""
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workgroup_assignment_named_workloads(msa, cfg):
     inst = make_layout_only(cfg)
-    _, work, _ = msa.msa_plan_export(host_plan(msa, inst))
-    for q in _xcd_queues(work):
-        longest = {}
-        for g, n in q:
-            longest[g] = max(longest.get(g, 0), n)
-        seen, prev_g, prev_n = set(), None, None
-        for g, n in q:
-            if g != prev_g:
-                assert g not in seen, "a group's pieces are not adjacent"
-                if prev_g is not None:
-                    assert longest[g] <= longest[prev_g]
-                seen.add(g)
-            else:
-                assert n <= prev_n
-            prev_g, prev_n = g, n
-    if cfg == 5:
-        # every queue's first piece is the longest piece of that queue
-        assert all(q[0][1] == max(n for _, n in q) for q in _xcd_queues(work) if q)
+    plan = host_plan(msa, inst)
+    _, work, _ = msa.msa_plan_export(plan)
+    check_workgroups(work, plan.info(), inst.num_kv_heads)
+
+
+@pytest.mark.parametrize("case", PLAN_CASES)
+@pytest.mark.parametrize("split", [0, 64, 1024])
+@pytest.mark.parametrize("tile_flag", [0, 4, 8, 16])
+def test_workgroup_assignment_random(msa, case, split, tile_flag):
+    inst = workloads.make_random(keep_logical=False, **case)
+    plan = host_plan(msa, inst, kv_split_tokens=split, flags=tile_flag)
+    _, work, _ = msa.msa_plan_export(plan)
+    if len(work):
+        check_workgroups(work, plan.info(), inst.num_kv_heads)
 
 
 def _descriptors(kv_lens, segs, hq, hkv, d):

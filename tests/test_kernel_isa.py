@@ -4,7 +4,8 @@ The kernels' speed rests on properties of the generated code that a compiler
 change could silently undo.  These tests compile the sources the way the
 build does and check them in the assembly and the resource report:
 
-* no kernel spills registers or uses scratch memory;
+* no kernel spills vector registers or uses scratch memory (at most two
+  scalar registers may go to VGPR lanes);
 * the attention kernels keep two waves per SIMD (their tiles assume it;
   32-row tiles need two workgroups per CU);
 * in the attention kernels the MFMA operand reads run ahead: most LDS waits
@@ -69,7 +70,10 @@ def test_no_spills_or_scratch(compiled, src):
     kernels = _resources(compiled[src][1])
     assert kernels, "no resource remarks parsed"
     for name, r in kernels.items():
-        assert r.get("VGPRs Spill", 0) == 0 and r.get("SGPRs Spill", 0) == 0, (name, r)
+        # a scalar spill lands in a VGPR lane (no memory); the persistent
+        # attention loop keeps the launch arguments in SGPRs and may push one
+        # of them out once per workgroup
+        assert r.get("VGPRs Spill", 0) == 0 and r.get("SGPRs Spill", 0) <= 2, (name, r)
         assert r.get("ScratchSize", 0) == 0, (name, r)
 
 
