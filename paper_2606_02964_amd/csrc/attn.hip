@@ -1,8 +1,9 @@
 // attn.hip -- gfx950 kernels of Multi-Segment Attention.
 //
-// msa_attn: one workgroup of W waves (W = 4 or 8: 128 or 256 rows, 32 rows
-// per wave) per work item: query rows of one sequence sharing one KV head,
-// over one key range.  Each 64-key step:
+// msa_attn: workgroups of W waves (W = 4 or 8: 128 or 256 rows, 32 rows per
+// wave), each running its own list of work items (the launch is persistent;
+// the plan deals the items out).  A work item is query rows of one sequence
+// sharing one KV head, over one key range.  Each 64-key step:
 //   - paged gather: the step's 4 cache blocks are looked up in the block
 //     table (ids preloaded one lane per step, read with v_readlane) and
 //     copied straight into LDS (global_load_lds,
@@ -607,8 +608,8 @@ __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
 // half-step and the V of its current one loading while it computes.  The
 // four partial softmax states (max, sum, O) are merged through LDS at the
 // end.  Arithmetic per half-step is that of the main kernel: S^T = K Q^T
-// with K's rows permuted (bits 2 and 3 swapped), the lazy reference max and
-// bf16 weights whose row sum uses the same rounded values.
+// with K's rows permuted (bits 2 and 3 swapped), the lazy reference max,
+// bf16 weights for the PV product and a row sum of the fp32 weights.
 template <int D>
 struct DecodeLds {
   static constexpr int kWaves = 4;
