@@ -10,10 +10,12 @@ Inputs are synthetic (seeded N(0,1) draws rounded to bf16) and resident in
 HBM before timing starts; the plan is built once outside the timed region
 (it serves every layer of a batch step).
 
-Timing: ``us_per_call`` is the mean of back-to-back calls on one set of K/V
-caches (warm); ``us_per_call_cold`` the mean of back-to-back calls cycling
-through ``--cold-layers`` distinct caches, so that no call finds its K/V in
-L2 or the infinity cache.
+Timing, after the W warm-up calls: first ``us_per_call_cold``, the mean of
+back-to-back calls cycling through ``--cold-layers`` distinct caches, so that
+no call finds its K/V in L2 or the infinity cache; then ``us_per_call`` (the
+headline), the mean of K back-to-back calls on one set of K/V caches (warm).
+Timing the rotation first keeps the shader clock's ramp over the first
+calls of a burst out of the warm figure, whatever W is.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -534,19 +536,12 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
-    log(f"warm: {ms * 1e3:.1f} us/call")
 
-    # Cold: back-to-back calls cycling through distinct K/V caches, as the
-    # layers of a model step do.  Each call's K/V was last touched
-    # cold_layers - 1 calls (> 256 MB of other K/V) earlier, so neither L2 nor
-    # the 256 MB infinity cache holds it; the GPU stays busy, as in serving.
+    # Cold (timed first, right after the warm-up): back-to-back calls
+    # cycling through distinct K/V caches, as the layers of a model step do.
+    # Each call's K/V was last touched cold_layers - 1 calls (> 256 MB of
+    # other K/V) earlier, so neither L2 nor the 256 MB infinity cache holds
+    # it; the GPU stays busy, as in serving.
     cold_ms = None
     if args.cold_layers > 1:
         caches = [(k, v)] + [(k.clone(), v.clone()) for _ in range(args.cold_layers - 1)]
@@ -564,6 +559,18 @@ def main():
         cold_ms = a.elapsed_time(b) / calls
         del caches
         log(f"cold ({args.cold_layers} K/V caches in rotation): {cold_ms * 1e3:.1f} us/call")
+    # Warm: back-to-back calls on one set of K/V caches, timed after the
+    # cold rotation (the GPU has then run cold_layers + max(steps,
+    # 2 * cold_layers) calls past the warm-up, and its clock has settled).
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    log(f"warm: {ms * 1e3:.1f} us/call")
+
     # Isolated calls, each after a 512 MB buffer write.  These read slower
     # than either loop above because the shader clock drops between
     # isolated launches (measured in-kernel: ~1.85-1.9 GHz against ~2.0 GHz
@@ -636,7 +643,8 @@ def main():
         "us_per_call": round(ms * 1e3, 1),
         "us_per_call_cold": round(cold_ms * 1e3, 1) if cold_ms else None,
         "cold_protocol": (f"back-to-back calls over {args.cold_layers} distinct K/V caches (each call's "
-                          "K/V evicted from L2 and the 256 MB infinity cache by the others)"
+                          "K/V evicted from L2 and the 256 MB infinity cache by the others), timed right "
+                          "after the warm-up; the warm calls are timed after them"
                           if cold_ms else None),
         "us_per_call_isolated": round(iso_ms * 1e3, 1) if iso_ms else None,
         "plan_ms": round(plan_ms, 2),
