@@ -460,6 +460,8 @@ def main():
     ap.add_argument("--isolated", action="store_true",
                     help="also time single calls, each after a 512 MB buffer write (extra launches)")
     ap.add_argument("--kv-split-tokens", type=int, default=0)
+    ap.add_argument("--precise-weights", action="store_true",
+                    help="plan with MSA_PLAN_PRECISE_WEIGHTS (hi + lo bf16 weights on every key step)")
     ap.add_argument("--decode-only", action="store_true",
                     help="keep only the decode rows of the workload (the sequences whose one segment is their "
                          "last token); the roofline is then HBM-bound")
@@ -522,7 +524,8 @@ def main():
                            inst.max_blocks_per_seq, inst.num_blocks, inst.scale)
     t0 = time.perf_counter()
     plan = msa.msa_plan(shape, inst.seq_kv_len, inst.seg_indptr, inst.seg_start, inst.seg_len,
-                        kv_split_tokens=args.kv_split_tokens, stream=stream)
+                        kv_split_tokens=args.kv_split_tokens,
+                        flags=msa.MSA_PLAN_PRECISE_WEIGHTS if args.precise_weights else 0, stream=stream)
     plan_ms = (time.perf_counter() - t0) * 1e3
     info = plan.info()
     log(f"plan: {info}")
@@ -594,6 +597,8 @@ def main():
     useful = info["useful_flops"]
     achieved = useful / (ms * 1e-3) / 1e12
     workload_name = workloads.CONFIG_DESCRIPTIONS[cfg] + f" (seed {cfg if args.seed is None else args.seed})"
+    if args.precise_weights:
+        workload_name += ", precise weights"
     if args.decode_only:
         # decode rows: bound by streaming their visible K/V once (per call,
         # the split merge included)
@@ -604,7 +609,8 @@ def main():
         gather = gather_rates(inst, k, v, stream, args.warmup, args.steps)
         log(f"plain gather of the same blocks: {gather}")
     else:
-        traffic = measured_traffic(workload_name) if info["num_merge"] == 0 else None
+        traffic = (measured_traffic(workload_name)
+                   if info["num_merge"] == 0 and not args.precise_weights else None)
         roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                     "traffic": traffic}
@@ -639,6 +645,7 @@ def main():
             "kernels_per_call": 1 + (1 if info["num_merge"] else 0),
             "work_items": info["num_work"],
             "tile_rows": info["tile_rows"],
+            "precise_weights": bool(args.precise_weights),
         },
         "us_per_call": round(ms * 1e3, 1),
         "us_per_call_cold": round(cold_ms * 1e3, 1) if cold_ms else None,

@@ -123,6 +123,17 @@ typedef struct msa_plan_opts {
 #define MSA_PLAN_TILE_ROWS_128 4
 #define MSA_PLAN_TILE_ROWS_256 8
 #define MSA_PLAN_TILE_ROWS_32 16
+/* Carry every softmax weight into the P.V product as two bf16 terms,
+ * hi = bf16(w) and lo = bf16(w - hi), as the default path does only on the
+ * key step that holds each row's own position.  By default the weights of
+ * earlier keys enter as bf16 numbers (each moved by up to 2^-8 of itself):
+ * on inputs whose scores make a few keys carry a row's weight, this moves
+ * the output by up to 2^-8 * sum_j p_j |v_j| (p_j the normalised weights)
+ * before its own bf16 rounding.  With this flag the weights hold to about
+ * 2^-17, at the cost of a second P.V product on every step and no
+ * software pipelining (about twice the time of a call).  The plan is
+ * otherwise the same. */
+#define MSA_PLAN_PRECISE_WEIGHTS 32
 
 /* Figures describing a plan. */
 typedef struct msa_plan_info_t {

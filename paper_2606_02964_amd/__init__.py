@@ -46,6 +46,7 @@ MSA_PLAN_NO_AUTO_SPLIT = 2
 MSA_PLAN_TILE_ROWS_128 = 4
 MSA_PLAN_TILE_ROWS_256 = 8
 MSA_PLAN_TILE_ROWS_32 = 16
+MSA_PLAN_PRECISE_WEIGHTS = 32
 MSA_TABLE_HOST = 0
 MSA_TABLE_DEVICE = 1
 MSA_NOALLOC_WORKSPACE_BYTES = 64 << 20

@@ -96,6 +96,7 @@ msa_status msa::forward_impl(const char* who, msa_plan_t plan, const void* q, co
   p.group = hp.group;
   p.tile_tokens = hp.tile_tokens;
   p.scale_log2 = s.scale * 1.4426950408889634f;
+  p.precise = hp.precise_weights ? 1 : 0;
   const int num_wg = hp.wg_ptr.empty() ? 0 : (int)hp.wg_ptr.size() - 1;
   int rc = msa::launch_attn(p, s.head_dim, hp.tile_rows, num_wg, hip_stream);
   if (rc != 0) return set_error(MSA_ERR_DEVICE, std::string(w + ": attention launch failed: ") +

@@ -137,7 +137,7 @@ constexpr float kSettleSum = 128.0f;
 // (2 steps).  Every wave leaves through the barrier that ends the item's
 // last step before its epilogue (registers only), so the next item may
 // refill the rings at once.
-template <int D, int W>
+template <int D, int W, bool kPrecise>
 __device__ __forceinline__ void attn_item(const AttnParams& p, const WorkItem w, char* smem) {
   using T = Tile<D>;
   constexpr int kRows = 32 * W;  // tile rows
@@ -502,8 +502,9 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, const WorkItem w,
     wait_dma<0>();
     lds_barrier();
   };
+  // (with precise weights every step runs unpipelined, below)
   int j = 0;
-  for (; j + 2 < nw && !need_mask(j + 2); j += 2) {
+  for (; !kPrecise && j + 2 < nw && !need_mask(j + 2); j += 2) {
     issue(j + 2, j + 1);
     fused(std::integral_constant<int, 0>{}, std::false_type{}, std::true_type{}, j);
     tail();
@@ -517,6 +518,7 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, const WorkItem w,
   // On a masked step (split: the diagonal step of some row of the wave) the
   // rows whose diagonal step it is also enter their weights' bf16 lo terms
   // (other rows: zeros), in a second PV pass after the usual one on pk.
+  // With precise weights every step is split and every row enters them.
   auto plain = [&](int jj, bool split) {
     uint32_t pk[16];
     float ls;
@@ -538,7 +540,7 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, const WorkItem w,
         const int ks = i / (D / 32), dt = i % (D / 32);
         uint32_t pl[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) pl[u] = lo_pair(0, 8 * ks + 2 * u, pk[4 * ks + u], own);
+        for (int u = 0; u < 4; ++u) pl[u] = lo_pair(0, 8 * ks + 2 * u, pk[4 * ks + u], own || kPrecise);
         const bf16x8 pc = __builtin_bit_cast(bf16x8, make_uint4(pl[0], pl[1], pl[2], pl[3]));
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vread(jj, i), pc, oacc[dt], 0, 0, 0);
       }
@@ -550,7 +552,7 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, const WorkItem w,
   };
   for (; j < n; ++j) {
     issue(j + 2, j + 1);
-    if (j < nw) plain(j, need_mask(j));
+    if (j < nw) plain(j, kPrecise || need_mask(j));
     tail();
   }
 
@@ -590,13 +592,13 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, const WorkItem w,
 }
 
 // Persistent launch: workgroup i runs the items wg_ptr[i] .. wg_ptr[i+1]-1.
-template <int D, int W>
+template <int D, int W, bool kPrecise>
 __global__ __launch_bounds__(64 * W, 2) void msa_attn_kernel(AttnParams p) {
   using T = Tile<D>;
   // K ring (2 steps) then V ring (2 steps); K runs one step ahead of V
   __shared__ __attribute__((aligned(1024))) char smem[2 * T::kBytesK + 2 * T::kBytesV];
   const int end = p.wg_ptr[blockIdx.x + 1];
-  for (int it = p.wg_ptr[blockIdx.x]; it < end; ++it) attn_item<D, W>(p, p.work[it], smem);
+  for (int it = p.wg_ptr[blockIdx.x]; it < end; ++it) attn_item<D, W, kPrecise>(p, p.work[it], smem);
 }
 
 // msa_decode: tiles of up to 32 rows (decode-like plans).  Every wave of the
@@ -620,7 +622,7 @@ struct DecodeLds {
 
 // One work item of msa_decode; the LDS merge area is reused by the next item
 // only after the barrier the caller places between items.
-template <int D>
+template <int D, bool kPrecise>
 __device__ __forceinline__ void decode_item(const AttnParams& p, const WorkItem w, DecodeLds<D>& lds) {
   constexpr int kWaves = DecodeLds<D>::kWaves, kHalf = 32;
   auto& mo = lds.mo;
@@ -743,14 +745,17 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const WorkItem 
     const int k0 = w.kv_lo + h * kHalf;
     // On a masked half-step (split) the rows whose diagonal half-step it is
     // also enter their weights' bf16 lo terms, as in the main kernel: a
-    // second PV pass on them follows.
-    const bool split = k0 + kHalf - 1 >= pmin;  // holds some row's position, or passes one
-    if (split) {
+    // second PV pass on them follows (with precise weights: on every
+    // half-step, for every row).
+    const bool masked = k0 + kHalf - 1 >= pmin;  // holds some row's position, or passes one
+    const bool split = masked || kPrecise;
+    if (masked) {
       const int lim = pos - k0 - hl * 8;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[e] = ((e >> 3) * 16 + (e & 7)) <= lim ? sc[e] : -__builtin_inff();
     }
     uint32_t pk[8];
+    uint32_t plo[kPrecise ? 8 : 1];  // precise weights: the lo terms, taken with the hi ones
     float ls;
     auto weights = [&]() {
       const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
@@ -760,6 +765,10 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const WorkItem 
         const float w0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm));
         const float w1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e + 1], c, nm));
         pk[e >> 1] = pack_bf16x2(w0, w1);
+        if constexpr (kPrecise) {
+          const bf16x2 hv = __builtin_bit_cast(bf16x2, pk[e >> 1]);
+          plo[e >> 1] = pack_bf16x2(w0 - (float)hv[0], w1 - (float)hv[1]);
+        }
         ls += w0 + w1;  // fp32 sum (no v_dot2: it stalls the MFMA stream)
       }
     };
@@ -781,7 +790,7 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const WorkItem 
       }
     }
     const bool own = pos >= k0 && pos < k0 + kHalf;  // the row's diagonal half-step
-    if (split) {  // the same weights in fp32, in place of the scores; hi(w) == pk
+    if (split && !kPrecise) {  // the same weights in fp32, in place of the scores; hi(w) == pk
       const float nm = m_ref == -__builtin_inff() ? 0.0f : -m_ref;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, nm));
@@ -800,8 +809,12 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const WorkItem 
         uint32_t pl[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const bf16x2 hv = __builtin_bit_cast(bf16x2, pk[4 * ks + u]);
-          pl[u] = own ? pack_bf16x2(sc[8 * ks + 2 * u] - (float)hv[0], sc[8 * ks + 2 * u + 1] - (float)hv[1]) : 0u;
+          if constexpr (kPrecise) {
+            pl[u] = plo[4 * ks + u];
+          } else {
+            const bf16x2 hv = __builtin_bit_cast(bf16x2, pk[4 * ks + u]);
+            pl[u] = own ? pack_bf16x2(sc[8 * ks + 2 * u] - (float)hv[0], sc[8 * ks + 2 * u + 1] - (float)hv[1]) : 0u;
+          }
         }
         const bf16x8 pc = __builtin_bit_cast(bf16x8, make_uint4(pl[0], pl[1], pl[2], pl[3]));
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pc, oacc[dt], 0, 0, 0);
@@ -877,13 +890,13 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const WorkItem 
   }
 }
 
-template <int D>
+template <int D, bool kPrecise>
 __global__ __launch_bounds__(256, 2) void msa_decode_kernel(AttnParams p) {
   __shared__ __attribute__((aligned(16))) DecodeLds<D> lds;
   const int end = p.wg_ptr[blockIdx.x + 1];
   for (int it = p.wg_ptr[blockIdx.x]; it < end; ++it) {
     if (it > p.wg_ptr[blockIdx.x]) __syncthreads();  // the previous item's merge reads are done
-    decode_item<D>(p, p.work[it], lds);
+    decode_item<D, kPrecise>(p, p.work[it], lds);
   }
 }
 
@@ -922,26 +935,34 @@ __global__ __launch_bounds__(256) void msa_merge_kernel(MergeParams p) {
   }
 }
 
+// The precise-weights forms are separate instantiations, so that the
+// default kernels carry no test of the flag.
+template <bool kPrecise>
+int launch_attn_form(const AttnParams& p, int head_dim, int tile_rows, int num_wg, hipStream_t s) {
+  if (head_dim == 128 && tile_rows == kTileRowsNarrow)
+    hipLaunchKernelGGL((msa_attn_kernel<128, 4, kPrecise>), dim3(num_wg), dim3(256), 0, s, p);
+  else if (head_dim == 128 && tile_rows == kTileRowsWide)
+    hipLaunchKernelGGL((msa_attn_kernel<128, 8, kPrecise>), dim3(num_wg), dim3(512), 0, s, p);
+  else if (head_dim == 64 && tile_rows == kTileRowsNarrow)
+    hipLaunchKernelGGL((msa_attn_kernel<64, 4, kPrecise>), dim3(num_wg), dim3(256), 0, s, p);
+  else if (head_dim == 64 && tile_rows == kTileRowsWide)
+    hipLaunchKernelGGL((msa_attn_kernel<64, 8, kPrecise>), dim3(num_wg), dim3(512), 0, s, p);
+  else if (head_dim == 128 && tile_rows == kTileRowsDecode)
+    hipLaunchKernelGGL((msa_decode_kernel<128, kPrecise>), dim3(num_wg), dim3(256), 0, s, p);
+  else if (head_dim == 64 && tile_rows == kTileRowsDecode)
+    hipLaunchKernelGGL((msa_decode_kernel<64, kPrecise>), dim3(num_wg), dim3(256), 0, s, p);
+  else
+    return (int)hipErrorInvalidValue;
+  return (int)hipGetLastError();
+}
+
 }  // namespace
 
 int launch_attn(const AttnParams& p, int head_dim, int tile_rows, int num_wg, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (num_wg <= 0) return 0;
-  if (head_dim == 128 && tile_rows == kTileRowsNarrow)
-    hipLaunchKernelGGL((msa_attn_kernel<128, 4>), dim3(num_wg), dim3(256), 0, s, p);
-  else if (head_dim == 128 && tile_rows == kTileRowsWide)
-    hipLaunchKernelGGL((msa_attn_kernel<128, 8>), dim3(num_wg), dim3(512), 0, s, p);
-  else if (head_dim == 64 && tile_rows == kTileRowsNarrow)
-    hipLaunchKernelGGL((msa_attn_kernel<64, 4>), dim3(num_wg), dim3(256), 0, s, p);
-  else if (head_dim == 64 && tile_rows == kTileRowsWide)
-    hipLaunchKernelGGL((msa_attn_kernel<64, 8>), dim3(num_wg), dim3(512), 0, s, p);
-  else if (head_dim == 128 && tile_rows == kTileRowsDecode)
-    hipLaunchKernelGGL(msa_decode_kernel<128>, dim3(num_wg), dim3(256), 0, s, p);
-  else if (head_dim == 64 && tile_rows == kTileRowsDecode)
-    hipLaunchKernelGGL(msa_decode_kernel<64>, dim3(num_wg), dim3(256), 0, s, p);
-  else
-    return (int)hipErrorInvalidValue;
-  return (int)hipGetLastError();
+  return p.precise ? launch_attn_form<true>(p, head_dim, tile_rows, num_wg, s)
+                   : launch_attn_form<false>(p, head_dim, tile_rows, num_wg, s);
 }
 
 int launch_merge(const MergeParams& p, int head_dim, int num_merge, void* stream) {

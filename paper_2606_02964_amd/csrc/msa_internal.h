@@ -72,6 +72,7 @@ struct AttnParams {
   int32_t group;     // G = Hq / Hkv
   int32_t tile_tokens;
   float scale_log2;  // scale * log2(e)
+  int32_t precise;   // nonzero: every step carries hi + lo weights (MSA_PLAN_PRECISE_WEIGHTS)
 };
 
 struct MergeParams {

@@ -74,7 +74,7 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   for (int i = 0; i < 5; ++i)
     if (o.reserved[i] != 0) return fail(err, MSA_ERR_INVALID_ARG, "opts.reserved must be zero");
   if (o.flags & ~(MSA_PLAN_HOST_ONLY | MSA_PLAN_NO_AUTO_SPLIT | MSA_PLAN_TILE_ROWS_128 |
-                  MSA_PLAN_TILE_ROWS_256 | MSA_PLAN_TILE_ROWS_32))
+                  MSA_PLAN_TILE_ROWS_256 | MSA_PLAN_TILE_ROWS_32 | MSA_PLAN_PRECISE_WEIGHTS))
     return fail(err, MSA_ERR_INVALID_ARG, "unknown opts.flags bits");
   {
     const int forced = !!(o.flags & MSA_PLAN_TILE_ROWS_128) + !!(o.flags & MSA_PLAN_TILE_ROWS_256) +
@@ -129,6 +129,7 @@ msa_status build_plan(const msa_shape* shape, const int32_t* seq_kv_len, const i
   P = HostPlan{};
   P.shape = s;
   P.group = G;
+  P.precise_weights = (o.flags & MSA_PLAN_PRECISE_WEIGHTS) != 0;
   std::vector<int64_t> seq_row0(B + 1, 0);
   std::vector<int32_t> seq_maxpos(B, -1);
   int64_t total = 0;

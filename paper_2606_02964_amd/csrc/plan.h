@@ -15,6 +15,7 @@ struct HostPlan {
   int32_t group = 1;        // G = Hq / Hkv
   int32_t tile_rows = 0;    // rows per tile: kTileRowsDecode, kTileRowsNarrow or kTileRowsWide
   int32_t tile_tokens = 0;  // query tokens per tile
+  bool precise_weights = false;  // MSA_PLAN_PRECISE_WEIGHTS: hi + lo weights on every step
   int64_t total_q = 0;
   std::vector<int32_t> row_pos;   // [total_q] absolute position of each packed row
   std::vector<int32_t> seq_blocks; // [num_seqs] block-table entries the plan reads per sequence

@@ -210,6 +210,21 @@ def test_plan_is_deterministic(msa):
         assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("tile_flag", [0, 4, 8, 16])
+def test_precise_weights_flag_leaves_the_plan_unchanged(msa, tile_flag):
+    """MSA_PLAN_PRECISE_WEIGHTS changes only the kernels' arithmetic: the
+    exported plan (positions, work items, merges) is the same; flag bits
+    beyond the documented ones are still refused."""
+    inst = workloads.make_random(keep_logical=False, **PLAN_CASES[1])
+    a = msa.msa_plan_export(host_plan(msa, inst, flags=tile_flag))
+    b = msa.msa_plan_export(host_plan(msa, inst, flags=tile_flag | msa.MSA_PLAN_PRECISE_WEIGHTS))
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    with pytest.raises(msa.MsaError) as e:
+        host_plan(msa, inst, flags=msa.MSA_PLAN_PRECISE_WEIGHTS << 1)
+    assert e.value.status == msa.MSA_ERR_INVALID_ARG
+
+
 def test_empty_and_zero_segment_sequences(msa):
     inst = workloads.make_layout(5, [10, 40, 0], [[], [(3, 5)], []], 4, 2, 64)
     plan = host_plan(msa, inst)

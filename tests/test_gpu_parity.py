@@ -22,7 +22,8 @@ if not torch.cuda.is_available():  # collected on a CPU-only host with -m gpu
     pytest.skip("no GPU visible", allow_module_level=True)
 
 from gpu_helpers import (LSE_ABS, MAX_ABS, MEAN_ABS, DeviceInstance, bf16_to_f32,  # noqa: E402
-                         check_o, dev_bf16, errors, run)
+                         check_o, dev_bf16, errors, log_parity, run)
+from tolerance import weight_rounding_bound  # noqa: E402
 import paper_2606_02964_amd as msa  # noqa: E402
 
 
@@ -86,16 +87,18 @@ def test_prefill_and_decode_layouts(oracle_lib, tile):
     check_full(inst, oracle_lib, flags=tile)
 
 
+@pytest.mark.parametrize("precise", [0, msa.MSA_PLAN_PRECISE_WEIGHTS])
 @pytest.mark.parametrize("case", [RANDOM[1], RANDOM[4], RANDOM[6]])
-def test_tile_width_is_bitwise_invariant(case):
+def test_tile_width_is_bitwise_invariant(case, precise):
     """A row's arithmetic does not depend on which rows share its tile, so
-    without key splits the 128-row and 256-row kernels agree bit for bit."""
+    without key splits the 128-row and 256-row kernels agree bit for bit
+    (with bf16 or precise weights alike)."""
     seed, B, Hq, Hkv, d, max_len, max_segs = case
     inst = workloads.make_random(seed, num_seqs=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d,
                                  max_len=max_len, max_segs=max_segs, keep_logical=False)
     dinst = DeviceInstance(inst)
-    o1, l1, p1 = run(dinst, flags=msa.MSA_PLAN_NO_AUTO_SPLIT | msa.MSA_PLAN_TILE_ROWS_128)
-    o2, l2, p2 = run(dinst, flags=msa.MSA_PLAN_NO_AUTO_SPLIT | msa.MSA_PLAN_TILE_ROWS_256)
+    o1, l1, p1 = run(dinst, flags=precise | msa.MSA_PLAN_NO_AUTO_SPLIT | msa.MSA_PLAN_TILE_ROWS_128)
+    o2, l2, p2 = run(dinst, flags=precise | msa.MSA_PLAN_NO_AUTO_SPLIT | msa.MSA_PLAN_TILE_ROWS_256)
     assert p1.info()["tile_rows"] == 128 and p2.info()["tile_rows"] == 256
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
     assert torch.equal(l1, l2)
@@ -192,6 +195,65 @@ def test_scores_that_start_far_below_and_jump(oracle_lib, tile):
     assert float(np.abs(lse.cpu().numpy().astype(np.float64) - rl).max()) <= bound
 
 
+PEAKY = [(303, 3, 32, 8, 128, 1500), (304, 4, 16, 16, 64, 900)]
+
+
+def _peaky_instance(case):
+    seed, B, hq, hkv, d, max_len = case
+    inst = workloads.make_random(seed, num_seqs=B, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                                 max_len=max_len, max_segs=6, keep_logical=False)
+    inst.q = workloads.f32_to_bf16_bits(workloads.bf16_bits_to_f32(inst.q) * np.float32(4.0))
+    return inst
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("case", PEAKY)
+def test_peaky_logits_precise_weights(oracle_lib, case, tile):
+    """The peaky-logit inputs below with MSA_PLAN_PRECISE_WEIGHTS: every
+    weight enters the PV product as hi + lo bf16 terms, and the plain bar
+    holds again."""
+    check_full(_peaky_instance(case), oracle_lib, flags=tile | msa.MSA_PLAN_PRECISE_WEIGHTS)
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("split", [0, 320])
+@pytest.mark.parametrize("case", [RANDOM[1], RANDOM[4], RANDOM[6]])
+def test_precise_weights_random(oracle_lib, case, split, tile):
+    seed, B, Hq, Hkv, d, max_len, max_segs = case
+    inst = workloads.make_random(seed, num_seqs=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d,
+                                 max_len=max_len, max_segs=max_segs, keep_logical=False)
+    check_full(inst, oracle_lib, kv_split_tokens=split, flags=tile | msa.MSA_PLAN_PRECISE_WEIGHTS)
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("case", PEAKY)
+def test_peaky_logits(oracle_lib, case, tile):
+    """Peaky logits (a stress case outside the five workloads): Q scaled by 4
+    (exact in bf16), so the scores of a row spread over about 6 log2 units and
+    a few keys carry most of its weight.  The weights of keys before a row's
+    diagonal step enter the PV product as bf16 numbers, which moves such a
+    row's output by up to 2^-8 sum_j p_j |v_j| before its own rounding; with
+    that rounding on top the plain 1e-2 is out of reach here (see
+    ``tolerance.weight_rounding_bound``).  Every element must lie within
+    that bound, computed from the oracle run on the same instance with |V|;
+    the mean-abs and lse bars are the usual ones."""
+    inst = _peaky_instance(case)
+    o, lse, _ = run(DeviceInstance(inst), flags=tile)
+    ro, rl = oracle_lib.forward(inst)
+    abs_v = copy.copy(inst)
+    abs_v.v_cache = inst.v_cache & np.uint16(0x7FFF)
+    ra, _ = oracle_lib.forward(abs_v)
+    go = bf16_to_f32(o).astype(np.float64)
+    err = np.abs(go - ro)
+    bound = weight_rounding_bound(ro, ra)
+    lerr = float(np.abs(lse.cpu().numpy().astype(np.float64) - rl).max())
+    log_parity(elements=int(go.size), plain_max=float(err.max()), mean=float(err.mean()),
+               lse_max=lerr, bound_use=float((err / bound).max()))
+    assert np.isfinite(go).all()
+    assert np.all(err <= bound), float((err / bound).max())
+    assert float(err.mean()) <= MEAN_ABS and lerr <= LSE_ABS
+
+
 # Oracle results of the last full-size workload, shared by the tests that run
 # it with different plans (one instance at a time: config 2 alone is 0.7 GB).
 _FULL = {}
@@ -218,19 +280,21 @@ def _full_oracle(oracle_lib, cfg):
     return _FULL[cfg]
 
 
-@pytest.mark.parametrize("cfg,tile", [(2, 0), (3, 0), (3, msa.MSA_PLAN_TILE_ROWS_32), (4, 0),
-                                      (5, 0), (5, msa.MSA_PLAN_TILE_ROWS_32), ("5-decode", 0)])
+@pytest.mark.parametrize("cfg,tile", [(2, 0), (3, 0), (3, msa.MSA_PLAN_TILE_ROWS_32),
+                                      (3, msa.MSA_PLAN_PRECISE_WEIGHTS), (4, 0), (5, 0),
+                                      (5, msa.MSA_PLAN_TILE_ROWS_32), ("5-decode", 0),
+                                      ("5-decode", msa.MSA_PLAN_PRECISE_WEIGHTS)])
 def test_named_workload_full_parity(oracle_lib, cfg, tile):
     """Full-size workloads in the benchmark's launch configuration (automatic
     plan; two of them also forced onto 32-row tiles, whose kernel then takes
-    prefill segments at full size), compared with the oracle on every output
+    prefill segments at full size; two also with precise weights), compared with the oracle on every output
     element and every lse; the long-context workload on every row for one
     query head per KV head (a different head of each group).  Every output
     is also finite and inside the convex hull of V."""
     inst, ro, rl, heads = _full_oracle(oracle_lib, cfg)
     d = DeviceInstance(inst)
     o, lse, plan = run(d, flags=tile)
-    if tile:
+    if tile & msa.MSA_PLAN_TILE_ROWS_32:
         assert plan.info()["tile_rows"] == 32
     go = o.float()
     assert torch.isfinite(go).all().item(), "some output rows were not written"

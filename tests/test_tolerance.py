@@ -78,3 +78,52 @@ def test_rejects_values_off_the_bf16_grid():
     import pytest
     with pytest.raises(ValueError):
         bf16_interval_distance(np.array([np.float32(1.0 + 2 ** -12)]), np.array([1.0]))
+
+
+def test_half_spacing_of_bf16():
+    from tolerance import half_spacing_bf16
+    x = np.array([1.0, 1.99, 2.0, 3.0, 0.75, -4.5, 2.0 ** -20])
+    want = np.array([2 ** -8, 2 ** -8, 2 ** -7, 2 ** -7, 2 ** -9, 2 ** -6, 2.0 ** -28])
+    assert np.array_equal(half_spacing_bf16(x), want)
+    # a correctly rounded value is within half a spacing
+    rng = np.random.default_rng(3)
+    r = rng.standard_normal(100000) * 3
+    assert np.all(np.abs(_bf16(r).astype(np.float64) - r) <= half_spacing_bf16(r))
+
+
+def _peaky_rows(rng, n, keys, d, qscale):
+    """Exact outputs, attention over |V|, and outputs with bf16 weights in the
+    numerator (fp32-exact row sums), rounded to bf16, for random peaky rows."""
+    q = rng.standard_normal((n, d)) * qscale
+    k = rng.standard_normal((n, keys, d))
+    v = _bf16(rng.standard_normal((n, keys, d))).astype(np.float64)
+    s = np.einsum("nd,nkd->nk", q, k) / np.sqrt(d)
+    w = np.exp(s - s.max(axis=1, keepdims=True))
+    p = w / w.sum(axis=1, keepdims=True)
+    exact = np.einsum("nk,nkd->nd", p, v)
+    absv = np.einsum("nk,nkd->nd", p, np.abs(v))
+    wb = _bf16(w).astype(np.float64)
+    stored = _bf16(np.einsum("nk,nkd->nd", wb, v) / w.sum(axis=1, keepdims=True))
+    return exact, absv, stored
+
+
+def test_weight_rounding_bound_holds_and_is_tight():
+    """Rows whose weight sits on a few keys (Q scaled by 4 and 8): bf16
+    weights with an exact row sum, then the output's own rounding, stay within
+    the bound everywhere; the largest element uses most of it, the plain bar
+    fails on some, and an error of twice the bound is caught."""
+    from tolerance import weight_rounding_bound
+    rng = np.random.default_rng(5)
+    worst_use, plain_max = 0.0, 0.0
+    for qscale in (4.0, 8.0):
+        for keys in (2, 3, 8, 64):
+            exact, absv, stored = _peaky_rows(rng, 2000, keys, 64, qscale)
+            bound = weight_rounding_bound(exact, absv)
+            err = np.abs(stored.astype(np.float64) - exact)
+            assert np.all(err <= bound)
+            worst_use = max(worst_use, float((err / bound).max()))
+            plain_max = max(plain_max, float(err[np.abs(exact) < GRID_LIMIT].max()))
+            bad = stored.astype(np.float64) + 2 * bound * np.sign(rng.standard_normal(bound.shape))
+            assert np.all(np.abs(bad - exact) > bound)
+    assert worst_use > 0.8
+    assert plain_max > MAX_ABS

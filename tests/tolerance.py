@@ -77,3 +77,32 @@ def errors(stored: np.ndarray, ref: np.ndarray):
 def raw_max_abs(stored: np.ndarray, ref: np.ndarray) -> float:
     """Largest plain |stored - ref| over every element, reported beside the bar."""
     return float(np.abs(stored.astype(np.float64) - ref).max()) if stored.size else 0.0
+
+
+# Peaky-logit stress inputs (scores spread over many log2 units, so that a
+# few keys carry a row's weight).  There the plain bar is out of reach of a
+# path that, like this one, enters the softmax weights into the PV product as
+# bf16 numbers: each weight moves by up to 2^-8 of itself (8 significant
+# bits, round to nearest), and with the row sum over the unrounded weights
+# the output before its own rounding lies within 2^-8 * sum_j p_j |v_j| of the
+# exact value (p_j: the exact normalised weights).  That sum is attention
+# over |V| with the same weights, which the oracle computes when handed |V|.
+# The bound adds the stored number's own rounding and a slack for the fp32
+# scores, exp2 and sums.
+WEIGHT_ROUNDING = 2.0 ** -8
+WEIGHT_BOUND_SLACK = 1e-4
+
+
+def half_spacing_bf16(x: np.ndarray) -> np.ndarray:
+    """Half the spacing of bf16 numbers at magnitude |x| (2^(e - 8) on the
+    binade [2^e, 2^(e+1)))."""
+    a = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), 2.0 ** -126)
+    return np.exp2(np.floor(np.log2(a)) - 8)
+
+
+def weight_rounding_bound(ref: np.ndarray, ref_abs_v: np.ndarray) -> np.ndarray:
+    """Per element bound on |stored - ref| for bf16 weights in the PV
+    product: ``ref`` the exact output, ``ref_abs_v`` the exact attention
+    over |V| with the same weights."""
+    pre = WEIGHT_ROUNDING * np.asarray(ref_abs_v, dtype=np.float64) + WEIGHT_BOUND_SLACK
+    return pre + half_spacing_bf16(np.abs(np.asarray(ref, dtype=np.float64)) + pre)
