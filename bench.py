@@ -196,6 +196,11 @@ def report_all(path: str, steps: int, warmup: int):
             ms = time_calls(lambda: msa.msa_forward(plan, q, k, v, bt, o, None, ws, stream=stream),
                             stream, warmup, steps)
             t = ms * 1e-3
+            # the same call with every weight carried as hi + lo terms
+            plan_p = msa.msa_plan(shape, inst.seq_kv_len, inst.seg_indptr, inst.seg_start, inst.seg_len,
+                                  flags=msa.MSA_PLAN_PRECISE_WEIGHTS, stream=stream)
+            ms_p = time_calls(lambda: msa.msa_forward(plan_p, q, k, v, bt, o, None, ws, stream=stream),
+                              stream, warmup, steps)
             # the layer's cache write of the same rows (fresh K/V into the paged cache)
             kn, vn = (dev_bf16(x) for x in workloads.make_fresh_kv(inst, 4242))
             ms_app = time_calls(lambda: msa.msa_kv_append(plan, kn, vn, bt, k, v, stream=stream),
@@ -215,6 +220,7 @@ def report_all(path: str, steps: int, warmup: int):
                 "work_items": info["num_work"], "split_tiles": info["num_merge"],
                 "tile_rows": info["tile_rows"],
                 "max_splits": info["max_splits"],
+                "precise_us_per_call": round(ms_p * 1e3, 1),
                 "append_us_per_call": round(ms_app * 1e3, 2),
                 "append_gbs": round(app_bytes / (ms_app * 1e-3) / 1e9, 1),
                 "append_frac_hbm": round(app_bytes / (ms_app * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
@@ -222,7 +228,7 @@ def report_all(path: str, steps: int, warmup: int):
             out.write(json.dumps(rec) + "\n")
             out.flush()
             log(f"report: {rec}")
-            del q, k, v, bt, o, ws, plan, kn, vn
+            del q, k, v, bt, o, ws, plan, plan_p, kn, vn
             torch.cuda.empty_cache()
 
 
