@@ -579,6 +579,16 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
     log(f"warm: {ms * 1e3:.1f} us/call")
+    # Per-call durations of a further back-to-back window (an event between
+    # calls), reported as their median beside the window mean above.
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for i in range(args.steps):
+        step()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    median_ms = float(np.median([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]))
+    log(f"warm, per-call median: {median_ms * 1e3:.1f} us/call")
 
     # Isolated calls, each after a 512 MB buffer write.  These read slower
     # than either loop above because the shader clock drops between
@@ -654,6 +664,7 @@ def main():
             "precise_weights": bool(args.precise_weights),
         },
         "us_per_call": round(ms * 1e3, 1),
+        "us_per_call_median": round(median_ms * 1e3, 1),
         "us_per_call_cold": round(cold_ms * 1e3, 1) if cold_ms else None,
         "cold_protocol": (f"back-to-back calls over {args.cold_layers} distinct K/V caches (each call's "
                           "K/V evicted from L2 and the 256 MB infinity cache by the others), timed right "
