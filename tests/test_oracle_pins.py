@@ -46,6 +46,19 @@ def test_oracle_matches_dense_causal_sdpa(oracle_lib, case):
     np.testing.assert_allclose(lse, rlse, rtol=0, atol=1e-12)
 
 
+@pytest.mark.parametrize("qscale", [4.0, 16.0])
+def test_oracle_matches_dense_on_peaky_logits(oracle_lib, qscale):
+    """Q scaled by a power of two (exact in bf16): scores spread over many
+    log2 units, weights sit on a few keys, and the max subtraction and the
+    float64 sums still give the dense result."""
+    inst = _rand(RANDOM_CASES[2], keep_logical=True)
+    inst.q = workloads.f32_to_bf16_bits(workloads.bf16_bits_to_f32(inst.q) * np.float32(qscale))
+    o, lse = oracle_lib.forward(inst)
+    ro, rlse = dense_reference(inst)
+    np.testing.assert_allclose(o, ro, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(lse, rlse, rtol=0, atol=1e-10)
+
+
 def test_oracle_config1_matches_dense(oracle_lib):
     inst = workloads.make_config(1, keep_logical=True)
     o, lse = oracle_lib.forward(inst)
