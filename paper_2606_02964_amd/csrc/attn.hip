@@ -42,6 +42,9 @@
 // workgroup split the tile's keys, read K and V straight into registers and
 // merge their softmax states through LDS (see the kernel); masked
 // half-steps carry their weights as hi + lo terms, as above.
+// Both kernels also come in a precise-weights form (kPrecise, selected by
+// the plan): every step, or half-step, carries every row's weights as
+// hi + lo terms, and the main kernel then runs every step unpipelined.
 // msa_merge: combines the per-split partials of a split tile by log-sum-exp.
 #include <hip/hip_runtime.h>
 
