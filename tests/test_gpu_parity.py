@@ -331,6 +331,27 @@ def test_longest_context_sampled_parity(oracle_lib):
     check_o(gsel, ro, lsel, rl)
 
 
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 16, 64)])
+def test_long_prefill_sampled_parity(oracle_lib, hq, hkv, d):
+    """A whole 32768-token prompt as one segment [0, 32768) (plain causal
+    prefill, FlashAttention's case, at Llama 3.1's 32K context): every tile
+    of the sequence, from the first (a few keys) to the last (the whole
+    context), in one launch; sampled items plus the first and last rows."""
+    L = 32768
+    inst = workloads.make_layout(43, [L], [[(0, L)]], hq, hkv, d, keep_logical=False)
+    o, lse, plan = run(DeviceInstance(inst))
+    go = o.float()
+    assert torch.isfinite(go).all().item() and torch.isfinite(lse).all().item()
+    rows, heads = _sample_items(inst, 200, seed=43)
+    edges = np.array([0, 1, 63, 64, L // 2, L - 2, L - 1], dtype=np.int64)
+    rows = np.r_[rows, edges]
+    heads = np.r_[heads, np.arange(edges.size, dtype=np.int32) * 5 % hq].astype(np.int32)
+    ro, rl = oracle_lib.forward(inst, rows=rows, heads=heads)
+    gsel = go[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    lsel = lse[torch.from_numpy(rows).cuda(), torch.from_numpy(heads).long().cuda()].cpu().numpy()
+    check_o(gsel, ro, lsel, rl)
+
+
 def test_large_decode_batch_sampled_parity(oracle_lib):
     """1024 sequences with one decode row each (contexts 64..2048 keys, one
     TP=4 rank of Llama-3.1-8B: 8 query heads, 2 KV heads), plus 4 prefill
